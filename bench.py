@@ -1,0 +1,195 @@
+"""Benchmark of the PnP-Nystra window-attention hot path on one MI355X.
+
+One step = one PnP-Nystra forward (landmark pooling, kernel blocks,
+pseudo-inverse, value products, normalisation -- the whole path, one fused
+launch) over the SwinIR-like layer: a 256x256x180 feature map in 8x8 windows,
+1024 windows x 6 heads, N = 64, d_h = 30, m = 16 landmarks, K = 6
+pseudo-inverse iterations, fp32 storage (a bf16 run of the same layer is
+reported alongside).  Inputs are synthetic (seeded) and resident in HBM; the
+steps rotate over enough copies of them (> 1 GiB) that no step is served from
+the 256 MB Infinity Cache.
+
+Prints ONE JSON line (rank 0, N = 1 GPU).
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E peak, GB/s
+ROTATE_BYTES = 1.2 * (1 << 30)  # working set cycled by the timed steps
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="c2")
+    ap.add_argument("--dtype", default="f32", choices=["f32", "bf16"])
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-exact", action="store_true", help="skip the exact-attention timing")
+    ap.add_argument("--no-alt", action="store_true", help="skip the other-dtype run")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    return ap.parse_args()
+
+
+class Case:
+    """Device copies of one workload, rotated across steps."""
+
+    def __init__(self, wl, dtype, q, k, v):
+        import torch
+        from paper_2506_08520_amd import workloads as W  # noqa: F401
+        tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+        self.wl, self.dtype = wl, dtype
+        self.io_bytes = wl.io_bytes(dtype)
+        self.nsets = max(2, math.ceil(ROTATE_BYTES / self.io_bytes))
+        base = [torch.from_numpy(x).to(tdt).cuda() for x in (q, k, v)]
+        self.sets = []
+        for i in range(self.nsets):
+            trip = base if i == 0 else [t.clone() for t in base]
+            self.sets.append((*trip, torch.empty_like(base[0])))
+
+
+def time_kernel(case, launch, steps, warmup):
+    """Warm up, then time exactly `steps` launches.  Returns (ms per step by
+    the host clock between synchronisations, mean per-launch kernel ms from
+    HIP events recorded on the launch stream)."""
+    import torch
+    stream = torch.cuda.current_stream()
+    for i in range(warmup):
+        launch(*case.sets[i % case.nsets], stream)
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    stops = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        starts[i].record(stream)
+        launch(*case.sets[(warmup + i) % case.nsets], stream)
+        stops[i].record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    kern = sum(a.elapsed_time(b) for a, b in zip(starts, stops)) / steps
+    return (t1 - t0) * 1e3 / steps, kern
+
+
+def cpu_baseline(wl, q, k, v, budget_s):
+    """The float64 oracle on a bounded sample of the same units: a strided
+    subset when the whole workload would overrun the budget, otherwise the
+    whole workload repeated until the budget is spent."""
+    import numpy as np
+    import oracle
+    units = wl.units
+    flat = [x.reshape(units, wl.N, wl.d) for x in (q, k, v)]
+    probe = min(units, 48)
+    idx = np.linspace(0, units - 1, probe).round().astype(np.int64)
+    t0 = time.perf_counter()
+    oracle.forward(*(x[idx] for x in flat), wl.m)
+    t_probe = time.perf_counter() - t0
+    per_unit = max(t_probe, 1e-6) / probe
+    n = int(min(units, max(probe, budget_s / per_unit)))
+    reps = max(1, int(budget_s / (per_unit * n))) if n == units else 1
+    idx = np.linspace(0, units - 1, n).round().astype(np.int64)
+    sample = [np.ascontiguousarray(x[idx]) for x in flat]
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        oracle.forward(*sample, wl.m)
+    dt = time.perf_counter() - t0
+    tokens = reps * n * wl.N / wl.heads   # spatial tokens (all heads) processed
+    what = (f"all {units} units x {reps} passes" if n == units
+            else f"{n} of {units} units, strided")
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": oracle.max_threads(),
+            "kind": "oracle",
+            "sample": f"{what} of {wl.name} ({wl.N} tokens, m={wl.m}, K=6); float64 C "
+                      f"oracle, {dt:.1f} s wall"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the method's "
+              "(window, head) units are independent, so N GPUs would each run 1/N of the "
+              "windows with no communication.", file=sys.stderr)
+        return 2
+    import torch
+    from paper_2506_08520_amd import binding as B
+    from paper_2506_08520_amd import workloads as W
+
+    B.lib()
+    wl = W.CONFIGS[args.config]
+    dtypes = [args.dtype] + ([] if args.no_alt else [d for d in wl.dtypes if d != args.dtype])
+    results = {}
+    main_inputs = None
+    for dt in dtypes:
+        q, k, v = W.generate(wl, dt)
+        if dt == args.dtype:
+            main_inputs = (q, k, v)
+        case = Case(wl, dt, q, k, v)
+
+        def nys(q_, k_, v_, o_, s):
+            B.nystra_attn_forward(q_, k_, v_, wl.m, out=o_, stream=s)
+
+        def ex(q_, k_, v_, o_, s):
+            B.nystra_exact_attn_forward(q_, k_, v_, out=o_, stream=s)
+
+        ms, kern = time_kernel(case, nys, args.steps, args.warmup)
+        r = {"ms_per_step": ms, "kernel_ms": kern, "io_bytes": case.io_bytes,
+             "variant": B.nystra_select_variant(wl.N, wl.d, wl.m,
+                                                B.F32 if dt == "f32" else B.BF16)}
+        if not args.no_exact:
+            ems, ekern = time_kernel(case, ex, max(10, args.steps // 4), args.warmup)
+            r.update(exact_ms_per_step=ems, exact_kernel_ms=ekern)
+        results[dt] = r
+        del case
+        torch.cuda.empty_cache()
+
+    r = results[args.dtype]
+    tokens = wl.n_windows * wl.N
+    achieved = r["io_bytes"] / (r["kernel_ms"] * 1e-3) / 1e9
+    line = {
+        "metric": "Nystrom window-attention tokens/s at 1 MI355X; % peak HBM BW; "
+                  "speedup vs exact",
+        "value": tokens / (r["ms_per_step"] * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": r["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {wl.description}; {args.dtype} storage, "
+                               "K=6 pseudo-inverse iterations, 2-D pooled landmarks",
+                   "n_windows": wl.n_windows, "heads": wl.heads, "N": wl.N, "d_h": wl.d,
+                   "m": wl.m, "storage": args.dtype},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None},
+    }
+    if "exact_kernel_ms" in r:
+        line["speedup_vs_exact"] = r["exact_kernel_ms"] / r["kernel_ms"]
+    line["kernel_ms"] = r["kernel_ms"]
+    for dt, rr in results.items():
+        if dt == args.dtype:
+            continue
+        ach = rr["io_bytes"] / (rr["kernel_ms"] * 1e-3) / 1e9
+        line[f"{dt}_storage"] = {
+            "value": tokens / (rr["ms_per_step"] * 1e-3), "ms_per_step": rr["ms_per_step"],
+            "kernel_ms": rr["kernel_ms"], "achieved_GBs": ach, "frac": ach / HBM_PEAK_GBS,
+            "speedup_vs_exact": (rr["exact_kernel_ms"] / rr["kernel_ms"]
+                                 if "exact_kernel_ms" in rr else None)}
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_baseline(wl, *main_inputs, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

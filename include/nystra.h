@@ -1,0 +1,144 @@
+/*
+ * nystra.h -- C ABI of the MI355X (gfx950) PnP-Nystra window-attention library.
+ *
+ * PnP-Nystra ("Plug-and-Play Linear Attention with Provable Guarantees for
+ * Training-Free Image Restoration") replaces softmax self-attention inside
+ * window-based restoration Transformers by a Nystrom approximation of the
+ * exponential kernel G = exp(Q K^T / sqrt(d)) (Eqs. (2)-(7)), computed in the
+ * row-max-stabilised form of Eq. (8) (Sec. 2.2), independently for every
+ * (window, head) pair -- a "unit".
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Tensors.  Q, K, V, O are caller-owned DEVICE buffers, contiguous as
+ *   [n_windows][heads][N][d_h] with element type `dtype` (NYSTRA_F32 = IEEE
+ *   binary32, NYSTRA_BF16 = bfloat16).  Tokens of a window are row-major over
+ *   its sqrt(N) x sqrt(N) pixel grid (SwinIR / Uformer window partition); the
+ *   value width equals d_h.  O has the input dtype; bf16 outputs are rounded
+ *   to nearest-even from an fp32 result.  All arithmetic is fp32.
+ * Streams.  `stream` is a hipStream_t (NULL = the null stream).  Work is
+ *   enqueued and the call returns at once; the library never synchronises,
+ *   allocates no device memory and keeps no mutable global state, so calls
+ *   on different streams may overlap.  Faults inside a kernel surface at the
+ *   caller's next synchronisation.
+ * Errors.  Every function returns an int status (nystra_status).  All
+ *   argument checks run before anything is enqueued, so on any error other
+ *   than NYSTRA_ERR_HIP no output is written.  n_windows == 0 or heads == 0
+ *   is a valid no-op (pointers may then be NULL).  NYSTRA_ERR_HIP reports a
+ *   failed launch; nystra_last_error() then holds the HIP message for the
+ *   calling thread.  Nothing throws or aborts across this boundary.
+ * Limits.  1 <= N <= 4096, 1 <= d_h <= 64, 1 <= m <= min(N, 64),
+ *   n_windows * heads <= 2^31 - 1, 0 <= pinv_iters <= 64.  Pointers must be
+ *   aligned to the element size.  O must not overlap Q, K or V (Q, K, V may
+ *   alias each other).
+ */
+#ifndef NYSTRA_H
+#define NYSTRA_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { NYSTRA_F32 = 0, NYSTRA_BF16 = 1 } nystra_dtype;
+
+/* Landmark selection, Step 1 of Algorithm 1: landmarks are the means of the
+ * tokens in non-overlapping pooling windows (Sec. 2.2).
+ *  NYSTRA_LM_POOL2D:    the sqrt(N) x sqrt(N) token window is cut into m equal
+ *                       rectangular patches on a g_r x g_c grid, g_c being the
+ *                       largest divisor of m with g_c^2 <= m such that g_c and
+ *                       g_r = m / g_c both divide sqrt(N); landmarks numbered
+ *                       row-major over the patch grid.  Square m gives plain
+ *                       2-D average pooling.  Requires N to be a square.
+ *  NYSTRA_LM_SEGMENT1D: m contiguous runs of N/m tokens (requires m | N). */
+typedef enum { NYSTRA_LM_POOL2D = 0, NYSTRA_LM_SEGMENT1D = 1 } nystra_landmark_mode;
+
+/* Kernel family used by nystra_attn_forward_ex.  AUTO picks the MFMA-tiled
+ * kernel when the shape is one it covers and the generic kernel otherwise;
+ * the other values force one (NYSTRA_ERR_UNSUPPORTED if it cannot run). */
+typedef enum {
+    NYSTRA_VARIANT_AUTO = 0,
+    NYSTRA_VARIANT_GENERIC = 1,
+    NYSTRA_VARIANT_TILED = 2
+} nystra_variant;
+
+typedef enum {
+    NYSTRA_OK = 0,
+    NYSTRA_ERR_NULL = 1,        /* a required pointer is NULL                  */
+    NYSTRA_ERR_SHAPE = 2,       /* sizes out of range or no pooling grid       */
+    NYSTRA_ERR_DTYPE = 3,       /* dtype not NYSTRA_F32 / NYSTRA_BF16          */
+    NYSTRA_ERR_ALIGN = 4,       /* pointer not aligned to the element size     */
+    NYSTRA_ERR_OVERLAP = 5,     /* O overlaps Q, K or V                        */
+    NYSTRA_ERR_UNSUPPORTED = 6, /* forced variant cannot run this shape        */
+    NYSTRA_ERR_HIP = 7,         /* kernel launch failed (see nystra_last_error) */
+    NYSTRA_ERR_ARG = 8          /* other bad argument (mode, iters, scale)     */
+} nystra_status;
+
+typedef struct nystra_opts {
+    int pinv_iters;    /* Step 4 iterations K, 0..64; default 6                */
+    int landmark_mode; /* nystra_landmark_mode; default NYSTRA_LM_POOL2D       */
+    float scale;       /* logit scale; <= 0 selects 1/sqrt(d_h) (default 0)     */
+    int variant;       /* nystra_variant; default NYSTRA_VARIANT_AUTO           */
+} nystra_opts;
+
+/* Fill *opts with the defaults above.  Returns NYSTRA_ERR_NULL for NULL. */
+int nystra_default_opts(nystra_opts *opts);
+
+/* PnP-Nystra forward (Algorithm 1, stabilised form Eq. (8)) with default
+ * options: K = 6 pseudo-inverse iterations, POOL2D landmarks, scale
+ * 1/sqrt(d_h).  For every unit:
+ *   Qbar, Kbar = pooled landmark queries / keys (m x d_h)            Step 1
+ *   m_L(i) = max_j (s Q Kbar^T)_ij,   G_L^n = exp(s Q Kbar^T - m_L)  Step 3
+ *   m_U(i) = max_j (s Qbar K^T)_ij,   G_U^n = exp(s Qbar K^T - m_U)  Step 3
+ *   G_A^n = exp(s Qbar Kbar^T - m_U)  (rows scaled by m_U)            Step 2
+ *   Z = K iterations of Z <- Z(13I - AZ(15I - AZ(7I - AZ)))/4 on
+ *       A = G_A^n from Z_0 = A^T / (||A||_1 ||A||_inf)                Step 4
+ *   O = (G_L^n Z G_U^n V) / (G_L^n Z G_U^n 1_N)  row-wise             Steps 5-7
+ * The products of Steps 5-6 are evaluated as G_L^n (Z (G_U^n [V | 1])),
+ * which equals the paper's (G_L^n Z)(G_U^n [V | 1]) in exact arithmetic.
+ * No epsilon is added to the denominator (Step 7). */
+int nystra_attn_forward(const void *Q, const void *K, const void *V, void *O,
+                        int n_windows, int heads, int N, int d_h, int m, int dtype,
+                        void *stream);
+
+/* As nystra_attn_forward with explicit options (opts == NULL: defaults). */
+int nystra_attn_forward_ex(const void *Q, const void *K, const void *V, void *O,
+                           int n_windows, int heads, int N, int d_h, int m, int dtype,
+                           const nystra_opts *opts, void *stream);
+
+/* Exact windowed softmax self-attention, Eq. (1), per unit:
+ *   O = softmax(scale Q K^T) V, with the row maximum subtracted inside the
+ *   softmax.  scale <= 0 selects 1/sqrt(d_h).  Same layout, limits and
+ *   conventions as nystra_attn_forward (no m). */
+int nystra_exact_attn_forward(const void *Q, const void *K, const void *V, void *O,
+                              int n_windows, int heads, int N, int d_h, int dtype,
+                              float scale, void *stream);
+
+/* Step 1 alone (landmark pooling, Sec. 2.2).  Writes the fp32 landmark
+ * queries and keys Qbar, Kbar, each [n_windows][heads][m][d_h], and, if
+ * `map` is not NULL, the int32[N] token -> landmark map (device memory).
+ * Qbar, Kbar must not overlap Q, K; they must be 4-byte aligned. */
+int nystra_landmark_pool(const void *Q, const void *K, float *Qbar, float *Kbar,
+                         int32_t *map, int n_windows, int heads, int N, int d_h, int m,
+                         int dtype, int mode, void *stream);
+
+/* Host-only: the token -> landmark map of Step 1 into map_host[N]. */
+int nystra_landmark_map(int N, int m, int mode, int32_t *map_host);
+
+/* Host-only: which kernel family nystra_attn_forward_ex would launch for
+ * this shape and options (NYSTRA_VARIANT_GENERIC or NYSTRA_VARIANT_TILED), or a
+ * negative nystra_status if the arguments are invalid. */
+int nystra_select_variant(int N, int d_h, int m, int dtype, const nystra_opts *opts);
+
+/* Static description of a status code. */
+const char *nystra_status_str(int status);
+
+/* Detail of the last NYSTRA_ERR_HIP on the calling thread ("" if none). */
+const char *nystra_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NYSTRA_H */

@@ -1,0 +1,309 @@
+// extern "C" boundary of libnystra: argument validation, option resolution,
+// kernel-family selection and launch.  Every check runs before anything is
+// enqueued; the layer allocates nothing and never synchronises.
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include "../../include/nystra.h"
+#include "internal.hpp"
+
+namespace nystra {
+
+bool make_geometry(int N, int m, int mode, Geometry *g)
+{
+    if (N < 1 || m < 1 || m > N)
+        return false;
+    if (mode == NYSTRA_LM_POOL2D) {
+        int w = int(sqrt(double(N)) + 0.5);
+        if (w * w != N)
+            return false;
+        int best = 0;
+        for (int gc = 1; gc * gc <= m; ++gc)
+            if (m % gc == 0 && w % gc == 0 && w % (m / gc) == 0)
+                best = gc;
+        if (best == 0)
+            return false;
+        *g = Geometry{w, w, w / (m / best), w / best, best};
+        return true;
+    }
+    if (mode == NYSTRA_LM_SEGMENT1D) {
+        if (N % m != 0)
+            return false;
+        *g = Geometry{1, N, 1, N / m, m};
+        return true;
+    }
+    return false;
+}
+
+size_t generic_lds_bytes(int m, int d);
+
+}  // namespace nystra
+
+using nystra::Problem;
+
+namespace {
+
+constexpr int kMaxN = 4096;
+constexpr int kMaxD = 64;
+constexpr int kMaxM = 64;
+constexpr int kMaxIters = 64;
+
+thread_local char g_last_error[256] = "";
+
+void set_last_error(const char *msg)
+{
+    strncpy(g_last_error, msg ? msg : "", sizeof(g_last_error) - 1);
+    g_last_error[sizeof(g_last_error) - 1] = '\0';
+}
+
+int dtype_bytes(int dtype) { return dtype == NYSTRA_F32 ? 4 : 2; }
+
+bool misaligned(const void *p, int bytes) { return (uintptr_t(p) % uintptr_t(bytes)) != 0; }
+
+bool overlaps(const void *a, int64_t an, const void *b, int64_t bn)
+{
+    const uintptr_t a0 = uintptr_t(a), b0 = uintptr_t(b);
+    return a0 < b0 + uintptr_t(bn) && b0 < a0 + uintptr_t(an);
+}
+
+// Shape, dtype and count checks shared by every device entry point.
+int check_common(int n_windows, int heads, int N, int d, int dtype, int64_t *units)
+{
+    if (dtype != NYSTRA_F32 && dtype != NYSTRA_BF16)
+        return NYSTRA_ERR_DTYPE;
+    if (n_windows < 0 || heads < 0 || N < 1 || N > kMaxN || d < 1 || d > kMaxD)
+        return NYSTRA_ERR_SHAPE;
+    const int64_t u = int64_t(n_windows) * int64_t(heads);
+    if (u > int64_t(INT32_MAX))
+        return NYSTRA_ERR_SHAPE;
+    *units = u;
+    return NYSTRA_OK;
+}
+
+// Pointer checks: non-null, element-aligned, O disjoint from the inputs.
+int check_tensors(const void *Q, const void *K, const void *V, const void *O, int64_t bytes,
+                  int ebytes)
+{
+    if (!Q || !K || !V || !O)
+        return NYSTRA_ERR_NULL;
+    if (misaligned(Q, ebytes) || misaligned(K, ebytes) || misaligned(V, ebytes) ||
+        misaligned(O, ebytes))
+        return NYSTRA_ERR_ALIGN;
+    if (overlaps(O, bytes, Q, bytes) || overlaps(O, bytes, K, bytes) ||
+        overlaps(O, bytes, V, bytes))
+        return NYSTRA_ERR_OVERLAP;
+    return NYSTRA_OK;
+}
+
+int finish_launch(hipError_t e)
+{
+    if (e != hipSuccess) {
+        set_last_error(hipGetErrorString(e));
+        return NYSTRA_ERR_HIP;
+    }
+    return NYSTRA_OK;
+}
+
+// Resolves options and the problem; does not touch device memory.
+int build_problem(const void *Q, const void *K, const void *V, void *O, int n_windows,
+                  int heads, int N, int d, int m, int dtype, const nystra_opts *opts,
+                  Problem *p, int *variant)
+{
+    nystra_opts o;
+    nystra_default_opts(&o);
+    if (opts)
+        o = *opts;
+    int64_t units = 0;
+    int rc = check_common(n_windows, heads, N, d, dtype, &units);
+    if (rc != NYSTRA_OK)
+        return rc;
+    if (m < 1 || m > N || m > kMaxM)
+        return NYSTRA_ERR_SHAPE;
+    if (o.pinv_iters < 0 || o.pinv_iters > kMaxIters || !isfinite(o.scale) ||
+        (o.landmark_mode != NYSTRA_LM_POOL2D && o.landmark_mode != NYSTRA_LM_SEGMENT1D) ||
+        o.variant < NYSTRA_VARIANT_AUTO || o.variant > NYSTRA_VARIANT_TILED)
+        return NYSTRA_ERR_ARG;
+    nystra::Geometry g;
+    if (!nystra::make_geometry(N, m, o.landmark_mode, &g))
+        return NYSTRA_ERR_SHAPE;
+    p->q = Q;
+    p->k = K;
+    p->v = V;
+    p->o = O;
+    p->units = units;
+    p->N = N;
+    p->d = d;
+    p->m = m;
+    p->iters = o.pinv_iters;
+    p->dtype = dtype;
+    p->scale = o.scale > 0.f ? o.scale : float(1.0 / sqrt(double(d)));
+    p->geo = g;
+    const bool tiled = nystra::tiled_supported(*p);
+    if (o.variant == NYSTRA_VARIANT_TILED && !tiled)
+        return NYSTRA_ERR_UNSUPPORTED;
+    *variant = (o.variant == NYSTRA_VARIANT_GENERIC || !tiled) ? NYSTRA_VARIANT_GENERIC
+                                                               : NYSTRA_VARIANT_TILED;
+    return NYSTRA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int nystra_default_opts(nystra_opts *opts)
+{
+    if (!opts)
+        return NYSTRA_ERR_NULL;
+    opts->pinv_iters = 6;
+    opts->landmark_mode = NYSTRA_LM_POOL2D;
+    opts->scale = 0.f;
+    opts->variant = NYSTRA_VARIANT_AUTO;
+    return NYSTRA_OK;
+}
+
+int nystra_attn_forward_ex(const void *Q, const void *K, const void *V, void *O, int n_windows,
+                           int heads, int N, int d_h, int m, int dtype, const nystra_opts *opts,
+                           void *stream)
+{
+    Problem p;
+    int variant = 0;
+    int rc = build_problem(Q, K, V, O, n_windows, heads, N, d_h, m, dtype, opts, &p, &variant);
+    if (rc != NYSTRA_OK)
+        return rc;
+    if (p.units == 0)
+        return NYSTRA_OK;
+    const int64_t bytes = p.units * N * d_h * dtype_bytes(dtype);
+    rc = check_tensors(Q, K, V, O, bytes, dtype_bytes(dtype));
+    if (rc != NYSTRA_OK)
+        return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (variant == NYSTRA_VARIANT_TILED)
+        return finish_launch(nystra::launch_tiled_forward(p, s));
+    return finish_launch(nystra::launch_generic_forward(p, s));
+}
+
+int nystra_attn_forward(const void *Q, const void *K, const void *V, void *O, int n_windows,
+                        int heads, int N, int d_h, int m, int dtype, void *stream)
+{
+    return nystra_attn_forward_ex(Q, K, V, O, n_windows, heads, N, d_h, m, dtype, nullptr,
+                                  stream);
+}
+
+int nystra_exact_attn_forward(const void *Q, const void *K, const void *V, void *O,
+                              int n_windows, int heads, int N, int d_h, int dtype, float scale,
+                              void *stream)
+{
+    int64_t units = 0;
+    int rc = check_common(n_windows, heads, N, d_h, dtype, &units);
+    if (rc != NYSTRA_OK)
+        return rc;
+    if (!isfinite(scale))
+        return NYSTRA_ERR_ARG;
+    if (units == 0)
+        return NYSTRA_OK;
+    const int64_t bytes = units * N * d_h * dtype_bytes(dtype);
+    rc = check_tensors(Q, K, V, O, bytes, dtype_bytes(dtype));
+    if (rc != NYSTRA_OK)
+        return rc;
+    Problem p{};
+    p.q = Q;
+    p.k = K;
+    p.v = V;
+    p.o = O;
+    p.units = units;
+    p.N = N;
+    p.d = d_h;
+    p.m = 0;
+    p.dtype = dtype;
+    p.scale = scale > 0.f ? scale : float(1.0 / sqrt(double(d_h)));
+    return finish_launch(nystra::launch_exact(p, static_cast<hipStream_t>(stream)));
+}
+
+int nystra_landmark_pool(const void *Q, const void *K, float *Qbar, float *Kbar, int32_t *map,
+                         int n_windows, int heads, int N, int d_h, int m, int dtype, int mode,
+                         void *stream)
+{
+    int64_t units = 0;
+    int rc = check_common(n_windows, heads, N, d_h, dtype, &units);
+    if (rc != NYSTRA_OK)
+        return rc;
+    if (m < 1 || m > N || m > kMaxM)
+        return NYSTRA_ERR_SHAPE;
+    if (mode != NYSTRA_LM_POOL2D && mode != NYSTRA_LM_SEGMENT1D)
+        return NYSTRA_ERR_ARG;
+    nystra::Geometry g;
+    if (!nystra::make_geometry(N, m, mode, &g))
+        return NYSTRA_ERR_SHAPE;
+    if (units == 0)
+        return NYSTRA_OK;
+    const int eb = dtype_bytes(dtype);
+    if (!Q || !K || !Qbar || !Kbar)
+        return NYSTRA_ERR_NULL;
+    if (misaligned(Q, eb) || misaligned(K, eb) || misaligned(Qbar, 4) || misaligned(Kbar, 4) ||
+        (map && misaligned(map, 4)))
+        return NYSTRA_ERR_ALIGN;
+    const int64_t in_bytes = units * N * d_h * eb, out_bytes = units * m * d_h * 4;
+    if (overlaps(Qbar, out_bytes, Q, in_bytes) || overlaps(Qbar, out_bytes, K, in_bytes) ||
+        overlaps(Kbar, out_bytes, Q, in_bytes) || overlaps(Kbar, out_bytes, K, in_bytes) ||
+        overlaps(Qbar, out_bytes, Kbar, out_bytes))
+        return NYSTRA_ERR_OVERLAP;
+    Problem p{};
+    p.q = Q;
+    p.k = K;
+    p.units = units;
+    p.N = N;
+    p.d = d_h;
+    p.m = m;
+    p.dtype = dtype;
+    p.geo = g;
+    return finish_launch(
+        nystra::launch_landmark_pool(p, Qbar, Kbar, map, static_cast<hipStream_t>(stream)));
+}
+
+int nystra_landmark_map(int N, int m, int mode, int32_t *map_host)
+{
+    if (mode != NYSTRA_LM_POOL2D && mode != NYSTRA_LM_SEGMENT1D)
+        return NYSTRA_ERR_ARG;
+    if (N < 1 || N > kMaxN || m < 1 || m > N || m > kMaxM)
+        return NYSTRA_ERR_SHAPE;
+    nystra::Geometry g;
+    if (!nystra::make_geometry(N, m, mode, &g))
+        return NYSTRA_ERR_SHAPE;
+    if (!map_host)
+        return NYSTRA_ERR_NULL;
+    for (int t = 0; t < N; ++t) {
+        const int r = t / g.cols, c = t % g.cols;
+        map_host[t] = (r / g.pr) * g.gc + c / g.pc;
+    }
+    return NYSTRA_OK;
+}
+
+int nystra_select_variant(int N, int d_h, int m, int dtype, const nystra_opts *opts)
+{
+    Problem p;
+    int variant = 0;
+    int rc = build_problem(nullptr, nullptr, nullptr, nullptr, 1, 1, N, d_h, m, dtype, opts, &p,
+                           &variant);
+    return rc == NYSTRA_OK ? variant : -rc;
+}
+
+const char *nystra_status_str(int status)
+{
+    switch (status) {
+    case NYSTRA_OK: return "ok";
+    case NYSTRA_ERR_NULL: return "null pointer";
+    case NYSTRA_ERR_SHAPE: return "shape out of range or no pooling grid";
+    case NYSTRA_ERR_DTYPE: return "unsupported dtype";
+    case NYSTRA_ERR_ALIGN: return "misaligned pointer";
+    case NYSTRA_ERR_OVERLAP: return "output overlaps an input";
+    case NYSTRA_ERR_UNSUPPORTED: return "forced kernel variant cannot run this shape";
+    case NYSTRA_ERR_HIP: return "HIP launch error";
+    case NYSTRA_ERR_ARG: return "invalid argument";
+    default: return "unknown status";
+    }
+}
+
+const char *nystra_last_error(void) { return g_last_error; }
+
+}  // extern "C"

@@ -1,0 +1,43 @@
+// Internal interfaces between the C-ABI dispatch layer and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace nystra {
+
+// Pooling grid of Step 1 (Sec. 2.2).  Token t = r * cols + c of the window
+// averages into landmark (r / pr) * gc + (c / pc).  The 1-D mode is the same
+// grid with a single row of N tokens.
+struct Geometry {
+    int rows, cols;  // token grid
+    int pr, pc;      // patch rows / columns
+    int gc;          // patches per grid row
+};
+
+// Returns false when (N, m, mode) has no pooling grid.
+bool make_geometry(int N, int m, int mode, Geometry *g);
+
+struct Problem {
+    const void *q, *k, *v;
+    void *o;
+    int64_t units;   // n_windows * heads
+    int N, d, m;
+    int iters;
+    int dtype;       // 0 = fp32, 1 = bf16
+    float scale;     // resolved logit scale (> 0)
+    Geometry geo;
+};
+
+// Each launcher enqueues on `stream` and returns hipGetLastError().
+hipError_t launch_generic_forward(const Problem &p, hipStream_t stream);
+hipError_t launch_landmark_pool(const Problem &p, float *qbar, float *kbar, int32_t *map,
+                                hipStream_t stream);
+hipError_t launch_exact(const Problem &p, hipStream_t stream);
+
+// MFMA-tiled Nystrom kernels.  tiled_supported() is a host-side test of
+// whether a shape has a tiled kernel; launch_tiled_forward() requires it.
+bool tiled_supported(const Problem &p);
+hipError_t launch_tiled_forward(const Problem &p, hipStream_t stream);
+
+}  // namespace nystra

@@ -1,0 +1,163 @@
+"""Host-side checks of the C ABI: exports, the host landmark map, and every
+argument-validation path.  No call here reaches a kernel launch, so these run
+without a GPU."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2506_08520_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "nystra.h")
+
+OK, ENULL, ESHAPE, EDTYPE, EALIGN, EOVERLAP, EUNSUP, EHIP, EARG = range(9)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(nystra_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    return B.lib()
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert len(names) >= 9
+    assert sorted(B.EXPORTS) == names
+    out = subprocess.run(["nm", "-D", "--defined-only", B.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (nystra_\w+)", out))
+    for n in names:
+        assert n in exported, n
+        assert hasattr(L, n)
+
+
+def test_library_links_no_torch():
+    out = subprocess.run(["ldd", B.LIB_PATH], capture_output=True, text=True).stdout
+    assert "torch" not in out and "c10" not in out
+
+
+@pytest.mark.parametrize("N,m,mode", [(64, 16, 0), (64, 8, 0), (256, 32, 0), (1024, 64, 0),
+                                      (64, 16, 1), (64, 8, 1), (256, 32, 1), (1024, 64, 1),
+                                      (36, 6, 0), (4096, 64, 0), (9, 9, 0), (16, 1, 0),
+                                      (4096, 64, 1), (100, 25, 0), (24, 6, 1)])
+def test_host_map_bit_exact_vs_oracle(N, m, mode):
+    np.testing.assert_array_equal(B.nystra_landmark_map(N, m, mode),
+                                  oracle.landmark_map(N, m, mode))
+
+
+def test_host_map_matches_hand_written(golden_maps):
+    for (N, m, mode), grid in golden_maps.items():
+        np.testing.assert_array_equal(B.nystra_landmark_map(N, m, mode), grid)
+
+
+def test_host_map_rejects_what_the_oracle_rejects():
+    for N, m, mode in [(63, 7, 0), (64, 3, 0), (64, 5, 1), (50, 5, 0), (64, 65, 0)]:
+        with pytest.raises(B.NystraError) as e:
+            B.nystra_landmark_map(N, m, mode)
+        assert e.value.status == ESHAPE
+    with pytest.raises(B.NystraError):
+        B.nystra_landmark_map(64, 16, 9)
+
+
+# A fake, well-aligned device address: validation rejects every call below
+# before anything would touch it.
+P = 1 << 20
+
+
+def fwd(L, q=P, k=P + (1 << 24), v=P + (2 << 24), o=P + (3 << 24), W=2, H=3, N=64, d=30, m=16,
+        dtype=0, opts=None):
+    po = ctypes.byref(opts) if opts is not None else None
+    return L.nystra_attn_forward_ex(q, k, v, o, W, H, N, d, m, dtype, po, None)
+
+
+def test_forward_validation(L):
+    assert fwd(L, dtype=2) == EDTYPE
+    assert fwd(L, dtype=-1) == EDTYPE
+    for kw in [dict(N=0), dict(N=4097), dict(d=0), dict(d=65), dict(m=0), dict(m=65, N=4096),
+               dict(m=65), dict(W=-1), dict(H=-2), dict(N=63, m=7), dict(N=64, m=3),
+               dict(W=1 << 16, H=1 << 16)]:
+        assert fwd(L, **kw) == ESHAPE, kw
+    seg = B.make_opts(landmark_mode=1)
+    assert fwd(L, N=64, m=5, opts=seg) == ESHAPE
+    for o in [B.make_opts(pinv_iters=-1), B.make_opts(pinv_iters=65), B.make_opts(landmark_mode=2),
+              B.make_opts(variant=3), B.make_opts(scale=float("nan")),
+              B.make_opts(scale=float("inf"))]:
+        assert fwd(L, opts=o) == EARG
+    assert fwd(L, q=None) == ENULL
+    assert fwd(L, o=None) == ENULL
+    assert fwd(L, q=P + 2) == EALIGN
+    assert fwd(L, o=P + (3 << 24) + 2) == EALIGN
+    assert fwd(L, dtype=1, v=P + (2 << 24) + 1) == EALIGN
+    # bf16 needs only 2-byte alignment: an odd-halfword O is fine for alignment,
+    # so the overlap check is what fails here
+    assert fwd(L, dtype=1, o=P + 2) == EOVERLAP
+    assert fwd(L, o=P + 100) == EOVERLAP
+    assert fwd(L, o=P + (1 << 24) - 4) == EOVERLAP   # tail of Q meets head of O
+    # empty batches are a no-op whatever the pointers
+    assert fwd(L, W=0, q=None, k=None, v=None, o=None) == OK
+    assert fwd(L, H=0, q=None, k=None, v=None, o=None) == OK
+
+
+def test_default_forward_validation(L):
+    r = L.nystra_attn_forward(P, P + (1 << 24), P + (2 << 24), None, 2, 3, 64, 30, 16, 0, None)
+    assert r == ENULL
+    r = L.nystra_attn_forward(P, P, P, P, 0, 3, 64, 30, 16, 0, None)
+    assert r == OK
+
+
+def test_exact_validation(L):
+    f = L.nystra_exact_attn_forward
+    q, k, v, o = P, P + (1 << 24), P + (2 << 24), P + (3 << 24)
+    assert f(q, k, v, o, 2, 3, 64, 30, 7, 0.0, None) == EDTYPE
+    assert f(q, k, v, o, 2, 3, 0, 30, 0, 0.0, None) == ESHAPE
+    assert f(q, k, v, o, 2, 3, 64, 65, 0, 0.0, None) == ESHAPE
+    assert f(q, k, v, o, 2, 3, 64, 30, 0, float("nan"), None) == EARG
+    assert f(None, k, v, o, 2, 3, 64, 30, 0, 0.0, None) == ENULL
+    assert f(q, k, v, q + 8, 2, 3, 64, 30, 0, 0.0, None) == EOVERLAP
+    assert f(q, k, v, o + 1, 2, 3, 64, 30, 1, 0.0, None) == EALIGN
+    assert f(None, None, None, None, 0, 3, 64, 30, 0, 0.0, None) == OK
+
+
+def test_landmark_pool_validation(L):
+    f = L.nystra_landmark_pool
+    q, k, qb, kb = P, P + (1 << 24), P + (2 << 24), P + (3 << 24)
+    assert f(q, k, qb, kb, None, 2, 3, 64, 30, 16, 4, 0, None) == EDTYPE
+    assert f(q, k, qb, kb, None, 2, 3, 64, 30, 3, 0, 0, None) == ESHAPE
+    assert f(q, k, qb, kb, None, 2, 3, 64, 30, 16, 0, 5, None) == EARG
+    assert f(q, k, None, kb, None, 2, 3, 64, 30, 16, 0, 0, None) == ENULL
+    assert f(q, k, qb + 2, kb, None, 2, 3, 64, 30, 16, 1, 0, None) == EALIGN
+    assert f(q, k, qb, kb, P + (4 << 24) + 2, 2, 3, 64, 30, 16, 0, 0, None) == EALIGN
+    assert f(q, k, q + 16, kb, None, 2, 3, 64, 30, 16, 0, 0, None) == EOVERLAP
+    assert f(q, k, qb, qb + 64, None, 2, 3, 64, 30, 16, 0, 0, None) == EOVERLAP
+    assert f(None, None, None, None, None, 0, 3, 64, 30, 16, 0, 0, None) == OK
+
+
+def test_status_strings_and_opts(L):
+    for s in range(9):
+        assert B.nystra_status_str(s) and B.nystra_status_str(s) != "unknown status"
+    assert B.nystra_status_str(99) == "unknown status"
+    o = B.nystra_default_opts()
+    assert (o.pinv_iters, o.landmark_mode, o.scale, o.variant) == (6, 0, 0.0, 0)
+    assert L.nystra_default_opts(None) == ENULL
+    assert L.nystra_last_error() == b""
+
+
+def test_variant_selection():
+    g = B.VARIANT_GENERIC
+    assert B.nystra_select_variant(64, 30, 16, opts=B.make_opts(variant=g)) == g
+    assert B.nystra_select_variant(49, 64, 7) in (B.VARIANT_GENERIC, B.VARIANT_TILED)
+    with pytest.raises(B.NystraError):
+        B.nystra_select_variant(63, 30, 7)
+    with pytest.raises(B.NystraError):
+        B.nystra_select_variant(64, 30, 16, opts=B.make_opts(pinv_iters=-3))
+

@@ -1,0 +1,224 @@
+"""GPU parity: the HIP path through the C ABI against the float64 oracle.
+
+Small cases are compared on every unit; the full-size workloads run in the
+launch configuration the benchmark times and are compared on a strided
+sample of units (first and last included).  Bars: fp32 max-abs <= 1e-4;
+bf16 max-abs <= 2e-2 x RMS of the oracle output; landmark maps bit-exact.
+"""
+import functools
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2506_08520_amd import binding as B
+from paper_2506_08520_amd import workloads as W
+from helpers import TOL, error, sample_units, to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+VARIANTS = [B.VARIANT_GENERIC, B.VARIANT_TILED]
+
+
+def run(q, k, v, m, dtype, variant, iters=6, mode=0, scale=0.0):
+    shape = q.shape
+    tq, tk, tv = (to_dev(x, dtype) for x in (q, k, v))
+    opts = B.make_opts(pinv_iters=iters, landmark_mode=mode, scale=scale, variant=variant)
+    o = B.nystra_attn_forward_ex(tq, tk, tv, m, opts=opts)
+    torch.cuda.synchronize()
+    out = to_host(o)
+    assert out.shape == shape
+    return out
+
+
+def need_variant(N, d, m, dtype, variant, mode=0):
+    code = B.F32 if dtype == "f32" else B.BF16
+    if variant == B.VARIANT_TILED:
+        sel = B.nystra_select_variant(N, d, m, code, B.make_opts(landmark_mode=mode))
+        if sel != B.VARIANT_TILED:
+            pytest.skip("no MFMA-tiled kernel covers this shape; the generic kernel runs it")
+
+
+SMALL = [("c1", "f32", 4), ("c2", "f32", 4), ("c2", "bf16", 4), ("c3", "bf16", 16),
+         ("c4", "f32", 4), ("c4", "bf16", 4), ("c5", "bf16", 1)]
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("cfg,dtype,nw", SMALL)
+def test_config_shapes_all_units(cfg, dtype, nw, variant):
+    wl = W.CONFIGS[cfg]
+    need_variant(wl.N, wl.d, wl.m, dtype, variant)
+    q, k, v = W.generate(wl, dtype, n_windows=nw)
+    ref = oracle.forward(q, k, v, wl.m, iters=6, mode=0)
+    got = run(q, k, v, wl.m, dtype, variant)
+    err = error(got, ref, dtype)
+    print(f"{cfg} {dtype} variant={variant} err={err:.3e}")
+    assert err <= TOL[dtype]
+
+
+# (n_windows, heads, N, d, m, mode): ragged, degenerate and maximum shapes.
+EDGE = [
+    (3, 2, 36, 7, 6, 0),      # 6x6 window, 2x3 patches, odd width
+    (2, 1, 9, 1, 9, 0),       # m = N, d = 1
+    (2, 3, 64, 64, 64, 0),    # m = N = 64, widest head
+    (1, 2, 4096, 64, 64, 0),  # largest window and head
+    (5, 1, 64, 30, 1, 0),     # one landmark
+    (2, 2, 100, 16, 25, 0),   # 10x10 window, 2x2 patches
+    (2, 2, 48, 12, 12, 1),    # non-square N with 1-D segments
+    (3, 1, 64, 32, 8, 1),     # 1-D segments at a config shape
+    (1, 1, 1, 1, 1, 0),       # a single token: O = V
+    (7, 3, 16, 5, 4, 0),      # tiny window, many units
+    (2, 2, 256, 30, 16, 0),   # fewer landmarks at N = 256
+    (1, 3, 1024, 30, 32, 0),  # m = 32 at N = 1024
+]
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", EDGE, ids=lambda s: "x".join(map(str, s)))
+def test_edge_shapes(shape, dtype, variant):
+    nw, h, N, d, m, mode = shape
+    need_variant(N, d, m, dtype, variant, mode)
+    q, k, v = W.iid((nw, h, N, d), seed=N * 131 + d * 7 + m + mode, dtype=dtype)
+    ref = oracle.forward(q, k, v, m, iters=6, mode=mode)
+    got = run(q, k, v, m, dtype, variant, mode=mode)
+    assert error(got, ref, dtype, storage_floor=True) <= TOL[dtype]
+    if N == 1:
+        np.testing.assert_allclose(got, v, rtol=0, atol=1e-6 if dtype == "f32" else 1e-2)
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("iters", [0, 1, 3, 5, 8])
+def test_iteration_counts(iters, variant):
+    """fp32 parity over the paper's iteration range and a little beyond (the
+    float32 sensitivity at larger counts is documented by a CPU test)."""
+    wl = W.CONFIGS["c1"]
+    need_variant(wl.N, wl.d, wl.m, "f32", variant)
+    q, k, v = W.generate(wl, "f32", n_windows=8)
+    ref = oracle.forward(q, k, v, wl.m, iters=iters)
+    got = run(q, k, v, wl.m, "f32", variant, iters=iters)
+    assert error(got, ref, "f32") <= TOL["f32"]
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+def test_custom_scale(variant):
+    need_variant(64, 30, 16, "f32", variant)
+    q, k, v = W.iid((4, 2, 64, 30), seed=77)
+    ref = oracle.forward(q, k, v, 16, scale=0.05)
+    got = run(q, k, v, 16, "f32", variant, scale=0.05)
+    assert error(got, ref, "f32") <= TOL["f32"]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("N,d,m,mode", [(64, 30, 16, 0), (64, 32, 8, 0), (256, 30, 32, 0),
+                                        (1024, 32, 64, 0), (64, 30, 16, 1), (36, 7, 6, 0),
+                                        (4096, 3, 64, 1)])
+def test_landmark_pool(N, d, m, mode, dtype):
+    q, k, _ = W.iid((3, 2, N, d), seed=N + m, dtype=dtype)
+    qb, kb, mp = B.nystra_landmark_pool(to_dev(q, dtype), to_dev(k, dtype), m, mode=mode)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(mp.cpu().numpy(), oracle.landmark_map(N, m, mode))
+    qb, kb = to_host(qb), to_host(kb)
+    for u in range(6):
+        w, h = divmod(u, 2)
+        tr = oracle.unit_trace(q[w, h], k[w, h], q[w, h], m, iters=0, mode=mode)
+        np.testing.assert_allclose(qb[w, h], tr["Qbar"], rtol=1e-6, atol=1e-6)
+        np.testing.assert_allclose(kb[w, h], tr["Kbar"], rtol=1e-6, atol=1e-6)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [(4, 6, 64, 30), (16, 1, 64, 32), (2, 3, 256, 30),
+                                   (1, 4, 1024, 32), (3, 2, 36, 7), (2, 1, 1, 1),
+                                   (1, 2, 4096, 8), (2, 2, 64, 64)])
+def test_exact_kernel(shape, dtype):
+    q, k, v = W.iid(shape, seed=sum(shape), dtype=dtype)
+    ref = oracle.exact(q, k, v)
+    o = B.nystra_exact_attn_forward(*(to_dev(x, dtype) for x in (q, k, v)))
+    torch.cuda.synchronize()
+    assert error(to_host(o), ref, dtype, storage_floor=True) <= TOL[dtype]
+
+
+def test_exact_kernel_constant_values():
+    q, k, _ = W.iid((2, 3, 256, 30), seed=5)
+    v = np.ones_like(q)
+    o = B.nystra_exact_attn_forward(*(to_dev(x, "f32") for x in (q, k, v)))
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(to_host(o), 1.0, rtol=0, atol=1e-6)
+
+
+# ------------------------------------------------- full-size workloads ----
+
+@functools.lru_cache(maxsize=2)
+def full_inputs(cfg, dtype):
+    return W.generate(W.CONFIGS[cfg], dtype)
+
+
+FULL = [("c1", "f32", 384), ("c2", "f32", 192), ("c2", "bf16", 192), ("c3", "bf16", 256),
+        ("c4", "f32", 96), ("c4", "bf16", 96), ("c5", "bf16", 24)]
+
+
+@pytest.mark.parametrize("cfg,dtype,count", FULL)
+def test_full_size_sampled(cfg, dtype, count):
+    """The full workload in the benchmark's launch configuration (AUTO
+    variant, default options), checked on sampled units."""
+    wl = W.CONFIGS[cfg]
+    q, k, v = full_inputs(cfg, dtype)
+    tq, tk, tv = (to_dev(x, dtype) for x in (q, k, v))
+    o = B.nystra_attn_forward(tq, tk, tv, wl.m)
+    torch.cuda.synchronize()
+    got = to_host(o).reshape(wl.units, wl.N, wl.d)
+    idx = sample_units(wl.units, count)
+    ref = oracle.forward(*(x.reshape(-1, wl.N, wl.d)[idx] for x in (q, k, v)), wl.m)
+    err = error(got[idx], ref, dtype)
+    assert np.isfinite(got).all()
+    print(f"full {cfg} {dtype}: err {err:.3e} on {len(idx)} units")
+    assert err <= TOL[dtype]
+
+
+@pytest.mark.parametrize("cfg,dtype,count", [("c2", "f32", 64), ("c4", "bf16", 16),
+                                             ("c5", "bf16", 8)])
+def test_full_size_exact_sampled(cfg, dtype, count):
+    wl = W.CONFIGS[cfg]
+    q, k, v = full_inputs(cfg, dtype)
+    o = B.nystra_exact_attn_forward(*(to_dev(x, dtype) for x in (q, k, v)))
+    torch.cuda.synchronize()
+    got = to_host(o).reshape(wl.units, wl.N, wl.d)
+    idx = sample_units(wl.units, count)
+    ref = oracle.exact(*(x.reshape(-1, wl.N, wl.d)[idx] for x in (q, k, v)))
+    assert error(got[idx], ref, dtype) <= TOL[dtype]
+
+
+# --------------------------------------------------------- behaviour ----
+
+def test_deterministic_and_stream_independent():
+    q, k, v = W.generate(W.CONFIGS["c2"], "f32", n_windows=16)
+    tq, tk, tv = (to_dev(x, "f32") for x in (q, k, v))
+    a = B.nystra_attn_forward(tq, tk, tv, 16)
+    b = B.nystra_attn_forward(tq, tk, tv, 16)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        c = B.nystra_attn_forward(tq, tk, tv, 16, stream=s)
+    s.synchronize()
+    torch.cuda.synchronize()
+    assert torch.equal(a, b) and torch.equal(a, c)
+
+
+def test_output_untouched_on_validation_error():
+    q, k, v = (to_dev(x, "f32") for x in W.iid((2, 2, 64, 30), seed=3))
+    o = torch.full_like(q, 7.0)
+    with pytest.raises(B.NystraError) as e:
+        B.nystra_attn_forward(q, k, v, 3, out=o)   # no pooling grid for m = 3
+    assert e.value.status == 2
+    with pytest.raises(B.NystraError):
+        B.nystra_attn_forward_ex(q, k, v, 16, opts=B.make_opts(pinv_iters=99), out=o)
+    torch.cuda.synchronize()
+    assert bool((o == 7.0).all())
+
+
+def test_empty_batch_is_noop():
+    q = torch.empty((0, 6, 64, 30), device="cuda")
+    o = B.nystra_attn_forward(q, q, q, 16)
+    assert o.numel() == 0
