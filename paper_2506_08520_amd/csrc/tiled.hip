@@ -1,10 +1,523 @@
-// MFMA-tiled PnP-Nystra kernels (placeholder until the tiled family lands).
+// MFMA-tiled PnP-Nystra kernel for small windows (N = 16, 32 or 64 tokens,
+// m <= 16 landmarks, d_h in {8, 16, 24, 30, 32}): one wavefront computes one (window, head)
+// unit entirely in registers, with every contraction on the fp32 matrix cores
+// (v_mfma_f32_16x16x4f32) and LDS used only for a few small exchanges.
+//
+// Register tile convention ("D-layout").  A 16x16 fp32 tile M lives in one
+// float4 per lane: lane (g = lane / 16, c = lane % 16) holds M[4g + i][c],
+// i = 0..3 -- the layout in which the MFMA returns its result.  Running the
+// 16-deep contraction as four MFMA steps in which lane group g supplies the
+// k-index 4g + s at step s, a D-layout tile can be fed back directly:
+//   mm16(LT, R) = L * R   when LT holds L^T and R holds R, both in D-layout.
+// So a product's result is immediately the right-hand operand of the next
+// product, and a matrix is usable as a left-hand operand once its transpose
+// is in D-layout.  The few transposes needed go through 1.25 KB of LDS.
+//
+// Contractions over the feature dimension (S_L, S_U, S_A) use eight MFMA
+// steps in which each lane group supplies a chunk of 8 consecutive features
+// of one token row, loaded straight from global memory in 16-byte pieces
+// (see load_chunk8).  All global loads are branch-free and in bounds, so the
+// compiler can keep every load of a unit in flight at once.
+#include "device_common.hpp"
 #include "internal.hpp"
 
 namespace nystra {
+namespace {
 
-bool tiled_supported(const Problem &) { return false; }
+typedef float f4 __attribute__((ext_vector_type(4)));
 
-hipError_t launch_tiled_forward(const Problem &, hipStream_t) { return hipErrorInvalidValue; }
+constexpr int kWavesPerBlock = 4;
+constexpr int kLdStride = 36;   // row stride (floats) of the landmark tiles in LDS
+constexpr int kTrStride = 20;   // row stride (floats) of the transpose scratch
+constexpr int kLdsPerWave = 2 * 16 * kLdStride + 16 * kTrStride + 64;
+
+__device__ inline f4 mfma4(float a, float b, f4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// L * R for 16x16 tiles, LT = L^T and R in D-layout.
+__device__ inline f4 mm16(f4 LT, f4 R)
+{
+    f4 acc = {0.f, 0.f, 0.f, 0.f};
+    acc = mfma4(LT[0], R[0], acc);
+    acc = mfma4(LT[1], R[1], acc);
+    acc = mfma4(LT[2], R[2], acc);
+    acc = mfma4(LT[3], R[3], acc);
+    return acc;
+}
+
+// Orders the LDS traffic of one wavefront (all lanes execute in lockstep, so
+// only the compiler and the memory counters need fencing).
+__device__ inline void wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// D-layout transpose through the wave's LDS scratch.
+__device__ inline f4 transpose16(f4 M, float *scr, int g, int c)
+{
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        scr[(4 * g + i) * kTrStride + c] = M[i];
+    wave_sync();
+    f4 r = *reinterpret_cast<const f4 *>(scr + c * kTrStride + 4 * g);
+    wave_sync();
+    return r;
+}
+
+// Per-token vector exchange: value x (held per lane column c, identical in
+// all four lane groups) returned at row positions 4g + i.
+__device__ inline f4 by_rows(float x, float *vec, int g, int c)
+{
+    if (g == 0)
+        vec[c] = x;
+    wave_sync();
+    f4 r = *reinterpret_cast<const f4 *>(vec + 4 * g);
+    wave_sync();
+    return r;
+}
+
+// ---- cross-lane operations (wave64; a "row" is 16 lanes) ------------------
+// DPP forms fuse into the consuming VALU instruction; swizzle and bpermute
+// go through the LDS crossbar without touching LDS memory.
+
+__device__ inline float dpp_xor1(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0xB1, 0xF, 0xF, false); }
+__device__ inline float dpp_xor2(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0x4E, 0xF, 0xF, false); }
+__device__ inline float dpp_ror4(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0x124, 0xF, 0xF, false); }
+// Rotating a 16-lane row by 8 is the exchange of lanes c and c ^ 8.
+__device__ inline float dpp_xor8(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0x128, 0xF, 0xF, false); }
+__device__ inline float swz_xor4(float x)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x101F));
+}
+
+// Exchange with lane ^ 16 (swizzle inside each 32-lane half) and with
+// lane ^ 32 (permute through the LDS crossbar; no LDS memory is used).
+__device__ inline float swz_xor16(float x)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x401F));
+}
+
+__device__ inline float perm_xor32(float x)
+{
+    const int addr = int((__lane_id() ^ 32u) << 2);
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(addr, __builtin_bit_cast(int, x)));
+}
+
+// Sum / max over the four lanes c, c^16, c^32, c^48 (the lane groups g).
+__device__ inline float sum_groups(float x)
+{
+    x += swz_xor16(x);
+    return x + perm_xor32(x);
+}
+
+__device__ inline float max_groups(float x)
+{
+    x = fmaxf(x, swz_xor16(x));
+    return fmaxf(x, perm_xor32(x));
+}
+
+// Sum / max over the 16 lanes of a row.
+__device__ inline float sum_row(float x)
+{
+    x += dpp_xor1(x);
+    x += dpp_xor2(x);
+    x += dpp_ror4(x);
+    return x + dpp_xor8(x);
+}
+
+__device__ inline float max_row(float x)
+{
+    x = fmaxf(x, dpp_xor1(x));
+    x = fmaxf(x, dpp_xor2(x));
+    x = fmaxf(x, dpp_ror4(x));
+    return fmaxf(x, dpp_xor8(x));
+}
+
+struct __attribute__((aligned(4))) U16B {
+    uint32_t w[4];
+};
+
+// Feature chunk of lane group g.  The contraction over features runs as
+// eight MFMA steps in which group g supplies the features in slots s = 0..7.
+// Slot s of group g holds feature f0(g) + s with f0(g) = min(8g, D - 8), so a
+// chunk never reaches past its row; slots whose feature belongs to a lower
+// group (f0 + s < 8g) are zeroed.  D (>= 8) is a compile-time constant, so
+// every load is in bounds and the masks are plain selects.
+template <int D>
+__device__ inline int chunk_start(int g) { return min(8 * g, D - 8); }
+
+template <int D>
+__device__ inline bool slot_valid(int g, int s) { return chunk_start<D>(g) + s >= 8 * g; }
+
+template <class E, int D>
+__device__ inline void load_chunk8(const typename E::T *row, int g, float *out)
+{
+    static_assert(D >= 8, "tiled kernel needs at least 8 features");
+    const int f0 = chunk_start<D>(g);
+    if constexpr (E::bytes == 4) {
+        const U16B a = *reinterpret_cast<const U16B *>(row + f0);
+        const U16B b = *reinterpret_cast<const U16B *>(row + f0 + 4);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            out[j] = slot_valid<D>(g, j) ? __uint_as_float(a.w[j]) : 0.f;
+            out[4 + j] = slot_valid<D>(g, 4 + j) ? __uint_as_float(b.w[j]) : 0.f;
+        }
+    } else {
+        const U16B a = *reinterpret_cast<const U16B *>(row + f0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            out[2 * j] = slot_valid<D>(g, 2 * j) ? __uint_as_float(a.w[j] << 16) : 0.f;
+            out[2 * j + 1] =
+                slot_valid<D>(g, 2 * j + 1) ? __uint_as_float(a.w[j] & 0xffff0000u) : 0.f;
+        }
+    }
+}
+
+// Step 1 for one input: writes the patch means of this wave's tokens to
+// bar[l][f] (LDS).  A patch is the set of tokens that agree with its base
+// token outside the bit mask `free_bits` (the geometry is restricted to powers
+// of two): tile bits are summed within the lane, lane bits across lanes by
+// DPP / swizzle exchanges, one base tile (8 registers) at a time.
+template <int NT, int D>
+__device__ inline void pool_to_lds(const float (&x)[NT][8], float *bar, int free_bits,
+                                   int lg_cols, int lg_pr, int lg_pc, int lg_gc, float inv,
+                                   int g, int c)
+{
+    const int lane_bits = free_bits & 15, tile_bits = free_bits >> 4;
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt) {
+        if (tt & tile_bits)
+            continue;   // uniform: only base tiles of a patch produce a sum
+        float acc[8];
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+            acc[s] = x[tt][s];
+#pragma unroll
+        for (int u = 0; u < NT; ++u)
+            if (u != tt && ((u ^ tt) & ~tile_bits) == 0)
+#pragma unroll
+                for (int s = 0; s < 8; ++s)
+                    acc[s] += x[u][s];
+        if (lane_bits & 1)
+#pragma unroll
+            for (int s = 0; s < 8; ++s)
+                acc[s] += dpp_xor1(acc[s]);
+        if (lane_bits & 2)
+#pragma unroll
+            for (int s = 0; s < 8; ++s)
+                acc[s] += dpp_xor2(acc[s]);
+        if (lane_bits & 4)
+#pragma unroll
+            for (int s = 0; s < 8; ++s)
+                acc[s] += swz_xor4(acc[s]);
+        if (lane_bits & 8)
+#pragma unroll
+            for (int s = 0; s < 8; ++s)
+                acc[s] += dpp_xor8(acc[s]);
+        const int t = 16 * tt + c;
+        if ((t & free_bits) == 0) {
+            const int r = t >> lg_cols, cc = t & ((1 << lg_cols) - 1);
+            const int l = ((r >> lg_pr) << lg_gc) + (cc >> lg_pc);
+#pragma unroll
+            for (int s = 0; s < 8; ++s)
+                if (slot_valid<D>(g, s))
+                    bar[l * kLdStride + chunk_start<D>(g) + s] = acc[s] * inv;
+        }
+    }
+}
+
+struct SmallArgs {
+    int64_t units;
+    int m, iters;
+    float s2;          // logit scale in base-2 units (scale * log2 e)
+    float inv_patch;   // 1 / tokens per pooling patch
+    int lg_cols, lg_pr, lg_pc, lg_gc, free_bits;   // pooling grid (log2 sizes)
+};
+
+template <class E, int NT, int D>
+__global__ void __launch_bounds__(64 * kWavesPerBlock)
+tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__restrict__ k,
+                   const typename E::T *__restrict__ v, typename E::T *__restrict__ o,
+                   SmallArgs a)
+{
+    __shared__ float lds_all[kWavesPerBlock * kLdsPerWave];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int g = lane >> 4, c = lane & 15;
+    const int64_t unit = int64_t(blockIdx.x) * kWavesPerBlock + wave;
+    if (unit >= a.units)
+        return;   // whole wavefront; the kernel has no block-level barrier
+    constexpr int N = 16 * NT;
+    constexpr int d = D;
+    const int m = a.m;
+    float *qbar = lds_all + wave * kLdsPerWave;
+    float *kbar = qbar + 16 * kLdStride;
+    float *scr = kbar + 16 * kLdStride;
+    float *vec = scr + 16 * kTrStride;
+
+    const int64_t base = unit * int64_t(N) * d;
+    const typename E::T *qu = q + base, *ku = k + base, *vu = v + base;
+    typename E::T *ou = o + base;
+
+    // ---- Step 1: load token rows (features 8g..8g+7 of token 16tt+c) and pool.
+    float qr[NT][8], kr[NT][8];
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt) {
+        load_chunk8<E, D>(qu + int64_t(16 * tt + c) * d, g, qr[tt]);
+        load_chunk8<E, D>(ku + int64_t(16 * tt + c) * d, g, kr[tt]);
+    }
+    // V in the right-hand operand layout of T = G_U^n V: vr[tt][ct][s] =
+    // V[token 16tt+4g+s][feature 16ct+c] (zero past d).  Issued together with
+    // Q and K so that all of the unit's loads are in flight at once.
+    float vr[NT][2][4];
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+        for (int ct = 0; ct < 2; ++ct) {
+            const int f = 16 * ct + c;
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const float x = E::load(vu, int64_t(16 * tt + 4 * g + s) * d + min(f, d - 1));
+                vr[tt][ct][s] = f < d ? x : 0.f;
+            }
+        }
+    __builtin_amdgcn_sched_barrier(0);
+    // Landmark rows m..15 are padding: zero them so they contribute nothing.
+    for (int idx = lane; idx < (16 - m) * 32; idx += 64) {
+        const int r = m + idx / 32, f = idx % 32;
+        qbar[r * kLdStride + f] = 0.f;
+        kbar[r * kLdStride + f] = 0.f;
+    }
+    pool_to_lds<NT, D>(qr, qbar, a.free_bits, a.lg_cols, a.lg_pr, a.lg_pc, a.lg_gc,
+                       a.inv_patch, g, c);
+    pool_to_lds<NT, D>(kr, kbar, a.free_bits, a.lg_cols, a.lg_pr, a.lg_pc, a.lg_gc,
+                       a.inv_patch, g, c);
+    wave_sync();
+    float kb_a[8], qb_b[8];   // Kbar[c][f0 + s], Qbar[c][f0 + s] (slot layout)
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+        const bool ok = slot_valid<D>(g, s);
+        const int f = chunk_start<D>(g) + s;
+        kb_a[s] = ok ? kbar[c * kLdStride + f] : 0.f;
+        qb_b[s] = ok ? qbar[c * kLdStride + f] : 0.f;
+    }
+
+    // ---- Step 3, G_L side: S_L^T tiles, row max over landmarks, G_L^n.
+    // glT[tt] lane (g,c): G_L^n[token 16tt+c][landmark 4g+i].
+    f4 glT[NT];
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt) {
+        f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+            acc = mfma4(kb_a[s], qr[tt][s], acc);
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (4 * g + i < m)
+                mx = fmaxf(mx, acc[i]);
+        mx = a.s2 * max_groups(mx);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            glT[tt][i] = (4 * g + i < m) ? fast_exp2(fmaf(a.s2, acc[i], -mx)) : 0.f;
+    }
+
+    // ---- Step 3, G_U side: S_U^T tiles, row max over all N tokens, G_U^n.
+    // guT[tt] lane (g,c): G_U^n[landmark c][token 16tt+4g+i].
+    f4 guT[NT];
+    float mu = -INFINITY;
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt) {
+        f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+            acc = mfma4(kr[tt][s], qb_b[s], acc);
+        guT[tt] = acc;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            mu = fmaxf(mu, acc[i]);
+    }
+    mu = a.s2 * max_groups(mu);     // m_U of landmark c (base-2 units)
+    float tden = 0.f;                 // row sum of G_U^n for landmark c
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float e = (c < m) ? fast_exp2(fmaf(a.s2, guT[tt][i], -mu)) : 0.f;
+            guT[tt][i] = e;
+            tden += e;
+        }
+    tden = sum_groups(tden);
+
+    // ---- Step 6, first product: T = G_U^n V  (16 landmarks x 32 features).
+    // T[ct] lane (g,c): T[landmark 4g+i][feature 16ct+c].
+    f4 T[2];
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct) {
+        f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+                acc = mfma4(guT[tt][s], vr[tt][ct][s], acc);
+        T[ct] = acc;
+    }
+
+    // ---- Step 2: G_A^n (rows scaled by m_U).  AT lane (g,c): A[c][4g+i].
+    f4 AT;
+    {
+        f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+            acc = mfma4(kb_a[s], qb_b[s], acc);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            AT[i] = (c < m && 4 * g + i < m) ? fast_exp2(fmaf(a.s2, acc[i], -mu)) : 0.f;
+    }
+
+    // ---- Step 4: Z_0 = A^T / (||A||_1 ||A||_inf), then the iteration
+    //      X = A Z;  Z <- Z (13I - X (15I - X (7I - X))) / 4.
+    const float rowsum = sum_groups(AT[0] + AT[1] + AT[2] + AT[3]);   // sum_j A[c][j]
+    const float colsum = fmaxf(fmaxf(sum_row(AT[0]), sum_row(AT[1])),  // max_i sum_r A[r][4g+i]
+                               fmaxf(sum_row(AT[2]), sum_row(AT[3])));
+    const float norm_inf = max_groups(max_row(rowsum));
+    const float norm_1 = max_groups(colsum);
+    const float alpha = 1.0f / (norm_1 * norm_inf);
+    const f4 A = transpose16(AT, scr, g, c);
+    f4 Z = AT * alpha, ZT = A * alpha;
+    f4 eye;   // identity of the m x m block, D-layout
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        eye[i] = (4 * g + i == c && c < m) ? 1.f : 0.f;
+    for (int it = 0; it < a.iters; ++it) {
+        const f4 X = mm16(AT, Z);
+        const f4 XT = transpose16(X, scr, g, c);
+        f4 Y = eye * 7.f - X;
+        Y = eye * 15.f - mm16(XT, Y);
+        Y = eye * 13.f - mm16(XT, Y);
+        Z = mm16(ZT, Y) * 0.25f;
+        ZT = transpose16(Z, scr, g, c);
+    }
+
+    // ---- Steps 5-6 re-associated: W = Z T (and its denominator column).
+    f4 Wt[2];
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct)
+        Wt[ct] = mm16(ZT, T[ct]);
+    float wden;
+    {
+        const f4 td = by_rows(tden, vec, g, c);                    // T_D[4g+i]
+        wden = sum_groups(ZT[0] * td[0] + ZT[1] * td[1] + ZT[2] * td[2] + ZT[3] * td[3]);
+    }
+    const f4 wd = by_rows(wden, vec, g, c);                        // W_D[4g+i]
+
+    // ---- Steps 3 (G_L side), 6 and 7 per token tile: O = G_L^n W / O_D.
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt) {
+        const float od = sum_groups(glT[tt][0] * wd[0] + glT[tt][1] * wd[1] +
+                                      glT[tt][2] * wd[2] + glT[tt][3] * wd[3]);
+        const f4 odr = by_rows(od, vec, g, c);                     // O_D[16tt+4g+i]
+        f4 rcp;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            rcp[i] = __builtin_amdgcn_rcpf(odr[i]);
+#pragma unroll
+        for (int ct = 0; ct < 2; ++ct) {
+            const f4 on = mm16(glT[tt], Wt[ct]);
+            const int f = 16 * ct + c;
+            if (f < d) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    E::store(ou, int64_t(16 * tt + 4 * g + i) * d + f, on[i] * rcp[i]);
+            }
+        }
+    }
+}
+
+bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
+
+int ilog2(int x)
+{
+    int r = 0;
+    while ((1 << r) < x)
+        ++r;
+    return r;
+}
+
+template <class E, int NT, int D>
+void launch_small(const Problem &p, const SmallArgs &a, hipStream_t stream)
+{
+    const unsigned blocks = unsigned((p.units + kWavesPerBlock - 1) / kWavesPerBlock);
+    hipLaunchKernelGGL((tiled_small_kernel<E, NT, D>), dim3(blocks), dim3(64 * kWavesPerBlock),
+                       0, stream, static_cast<const typename E::T *>(p.q),
+                       static_cast<const typename E::T *>(p.k),
+                       static_cast<const typename E::T *>(p.v),
+                       static_cast<typename E::T *>(p.o), a);
+}
+
+template <class E, int D>
+void launch_small_d(const Problem &p, const SmallArgs &a, hipStream_t stream)
+{
+    switch (p.N) {
+    case 16: launch_small<E, 1, D>(p, a, stream); break;
+    case 32: launch_small<E, 2, D>(p, a, stream); break;
+    default: launch_small<E, 4, D>(p, a, stream); break;
+    }
+}
+
+// Head widths with a tiled instantiation.
+bool tiled_width(int d) { return d == 8 || d == 16 || d == 24 || d == 30 || d == 32; }
+
+template <class E>
+void launch_small_e(const Problem &p, const SmallArgs &a, hipStream_t stream)
+{
+    switch (p.d) {
+    case 8: launch_small_d<E, 8>(p, a, stream); break;
+    case 16: launch_small_d<E, 16>(p, a, stream); break;
+    case 24: launch_small_d<E, 24>(p, a, stream); break;
+    case 30: launch_small_d<E, 30>(p, a, stream); break;
+    default: launch_small_d<E, 32>(p, a, stream); break;
+    }
+}
+
+}  // namespace
+
+bool tiled_supported(const Problem &p)
+{
+    const Geometry &g = p.geo;
+    if (!(p.N == 16 || p.N == 32 || p.N == 64) || p.m > 16 || !tiled_width(p.d))
+        return false;
+    if (!is_pow2(g.cols) || !is_pow2(g.pr) || !is_pow2(g.pc) || !is_pow2(g.gc))
+        return false;
+    if (p.dtype == 1) {   // 16-byte row pieces of bf16 need 4-byte aligned rows
+        const uintptr_t mis = uintptr_t(p.q) | uintptr_t(p.k) | uintptr_t(p.v);
+        if (mis % 4 != 0)
+            return false;
+    }
+    return true;
+}
+
+hipError_t launch_tiled_forward(const Problem &p, hipStream_t stream)
+{
+    SmallArgs a;
+    a.units = p.units;
+    a.m = p.m;
+    a.iters = p.iters;
+    a.s2 = p.scale * kLog2e;
+    a.inv_patch = 1.0f / float(p.geo.pr * p.geo.pc);
+    a.lg_cols = ilog2(p.geo.cols);
+    a.lg_pr = ilog2(p.geo.pr);
+    a.lg_pc = ilog2(p.geo.pc);
+    a.lg_gc = ilog2(p.geo.gc);
+    a.free_bits = (p.geo.pc - 1) | ((p.geo.pr - 1) * p.geo.cols);
+    if (p.dtype == 0)
+        launch_small_e<F32>(p, a, stream);
+    else
+        launch_small_e<BF16>(p, a, stream);
+    return hipGetLastError();
+}
 
 }  // namespace nystra
