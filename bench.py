@@ -37,6 +37,9 @@ def parse():
     ap.add_argument("--no-exact", action="store_true", help="skip the exact-attention timing")
     ap.add_argument("--no-alt", action="store_true", help="skip the other-dtype run")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="also run a plain device-to-device copy of this many MiB (3 times), "
+                         "the reference kernel for scaling HBM byte counters")
     return ap.parse_args()
 
 
@@ -58,9 +61,12 @@ class Case:
 
 
 def time_kernel(case, launch, steps, warmup):
-    """Warm up, then time exactly `steps` launches.  Returns (ms per step by
-    the host clock between synchronisations, mean per-launch kernel ms from
-    HIP events recorded on the launch stream)."""
+    """Warm up, then time exactly `steps` launches.
+
+    Returns (ms per step by the host clock between synchronisations,
+    mean per-launch kernel ms from a HIP event pair around each launch, and
+    mean ms per launch from one event pair around all of them), all events
+    recorded on the stream the kernels are launched on."""
     import torch
     stream = torch.cuda.current_stream()
     for i in range(warmup):
@@ -76,7 +82,33 @@ def time_kernel(case, launch, steps, warmup):
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     kern = sum(a.elapsed_time(b) for a, b in zip(starts, stops)) / steps
-    return (t1 - t0) * 1e3 / steps, kern
+    # back-to-back launches between a single pair of events
+    r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    r0.record(stream)
+    for i in range(steps):
+        launch(*case.sets[(warmup + steps + i) % case.nsets], stream)
+    r1.record(stream)
+    torch.cuda.synchronize()
+    return (t1 - t0) * 1e3 / steps, kern, r0.elapsed_time(r1) / steps
+
+
+def measured_traffic(cfg, dtype, variant):
+    """HBM bytes per launch from the committed counter record, if the kernel
+    it was measured on is still the one in the source tree; else None."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if variant != 2 or not os.path.exists(path):
+        return None
+    rec = json.load(open(path)).get(f"{cfg}:{dtype}")
+    if rec is None:
+        return None
+    h = hashlib.sha256()
+    for f in rec["source_files"]:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    if h.hexdigest() != rec["source_sha256"]:
+        return None
+    return rec["fetch_bytes"] + rec["write_bytes"]
 
 
 def cpu_baseline(wl, q, k, v, budget_s):
@@ -94,13 +126,16 @@ def cpu_baseline(wl, q, k, v, budget_s):
     t_probe = time.perf_counter() - t0
     per_unit = max(t_probe, 1e-6) / probe
     n = int(min(units, max(probe, budget_s / per_unit)))
-    reps = max(1, int(budget_s / (per_unit * n))) if n == units else 1
     idx = np.linspace(0, units - 1, n).round().astype(np.int64)
     sample = [np.ascontiguousarray(x[idx]) for x in flat]
+    reps = 0
     t0 = time.perf_counter()
-    for _ in range(reps):
+    while True:   # whole passes until the budget is spent (at least one)
         oracle.forward(*sample, wl.m)
-    dt = time.perf_counter() - t0
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= budget_s or n < units:
+            break
     tokens = reps * n * wl.N / wl.heads   # spatial tokens (all heads) processed
     what = (f"all {units} units x {reps} passes" if n == units
             else f"{n} of {units} units, strided")
@@ -138,12 +173,12 @@ def main():
         def ex(q_, k_, v_, o_, s):
             B.nystra_exact_attn_forward(q_, k_, v_, out=o_, stream=s)
 
-        ms, kern = time_kernel(case, nys, args.steps, args.warmup)
-        r = {"ms_per_step": ms, "kernel_ms": kern, "io_bytes": case.io_bytes,
+        ms, kern, region = time_kernel(case, nys, args.steps, args.warmup)
+        r = {"ms_per_step": ms, "kernel_ms": kern, "region_ms": region, "io_bytes": case.io_bytes,
              "variant": B.nystra_select_variant(wl.N, wl.d, wl.m,
                                                 B.F32 if dt == "f32" else B.BF16)}
         if not args.no_exact:
-            ems, ekern = time_kernel(case, ex, max(10, args.steps // 4), args.warmup)
+            ems, ekern, _ = time_kernel(case, ex, max(10, args.steps // 4), args.warmup)
             r.update(exact_ms_per_step=ems, exact_kernel_ms=ekern)
         results[dt] = r
         del case
@@ -171,11 +206,15 @@ def main():
                    "n_windows": wl.n_windows, "heads": wl.heads, "N": wl.N, "d_h": wl.d,
                    "m": wl.m, "storage": args.dtype},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None},
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": measured_traffic(wl.name, args.dtype, r["variant"]),
+                     "algorithmic_bytes": r["io_bytes"]},
     }
     if "exact_kernel_ms" in r:
         line["speedup_vs_exact"] = r["exact_kernel_ms"] / r["kernel_ms"]
     line["kernel_ms"] = r["kernel_ms"]
+    line["kernel_ms_back_to_back"] = r["region_ms"]
+    line["variant"] = "mfma-tiled" if r["variant"] == 2 else "generic"
     for dt, rr in results.items():
         if dt == args.dtype:
             continue
@@ -185,6 +224,14 @@ def main():
             "kernel_ms": rr["kernel_ms"], "achieved_GBs": ach, "frac": ach / HBM_PEAK_GBS,
             "speedup_vs_exact": (rr["exact_kernel_ms"] / rr["kernel_ms"]
                                  if "exact_kernel_ms" in rr else None)}
+    if args.copy_mib > 0:
+        n = args.copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        line["copy_calibration_bytes"] = 2 * n * 4
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(wl, *main_inputs, args.cpu_seconds)
     print(json.dumps(line), flush=True)
