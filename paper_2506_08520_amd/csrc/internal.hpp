@@ -36,8 +36,15 @@ hipError_t launch_landmark_pool(const Problem &p, float *qbar, float *kbar, int3
 hipError_t launch_exact(const Problem &p, hipStream_t stream);
 
 // MFMA-tiled Nystrom kernels.  tiled_supported() is a host-side test of
-// whether a shape has a tiled kernel; launch_tiled_forward() requires it.
+// whether a shape has a tiled kernel; launch_tiled_forward() requires it and
+// picks the one-wave kernel for windows of at most 64 tokens and 16
+// landmarks, the multi-wave kernel otherwise.
 bool tiled_supported(const Problem &p);
 hipError_t launch_tiled_forward(const Problem &p, hipStream_t stream);
+bool tiled_large_supported(const Problem &p);
+hipError_t launch_tiled_large(const Problem &p, hipStream_t stream);
+
+// Head widths with a tiled instantiation.
+inline bool tiled_width(int d) { return d == 8 || d == 16 || d == 24 || d == 30 || d == 32; }
 
 }  // namespace nystra

@@ -1,0 +1,172 @@
+// Helpers shared by the MFMA-tiled kernels: the 16x16 register tile
+// convention, cross-lane exchanges and branch-free feature-chunk loads.
+//
+// Register tile convention ("D-layout").  A 16x16 fp32 tile M lives in one
+// float4 per lane: lane (g = lane / 16, c = lane % 16) holds M[4g + i][c],
+// i = 0..3 -- the layout in which v_mfma_f32_16x16x4f32 returns its result.
+// Running a 16-deep contraction as four MFMA steps in which lane group g
+// supplies the k-index 4g + s at step s, a D-layout tile can be fed back
+// directly:  mm16(LT, R) = L * R  when LT holds L^T and R holds R, both in
+// D-layout.  A product's result is immediately the right-hand operand of the
+// next product, and a matrix is usable as a left-hand operand once its
+// transpose is in D-layout.
+#pragma once
+
+#include "device_common.hpp"
+
+namespace nystra {
+namespace tile {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+constexpr int kLdStride = 36;   // row stride (floats) of the landmark tiles in LDS
+constexpr int kTrStride = 20;   // row stride (floats) of the transpose scratch
+
+__device__ inline f4 mfma4(float a, float b, f4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// L * R for 16x16 tiles, LT = L^T and R in D-layout.
+__device__ inline f4 mm16(f4 LT, f4 R)
+{
+    f4 acc = {0.f, 0.f, 0.f, 0.f};
+    acc = mfma4(LT[0], R[0], acc);
+    acc = mfma4(LT[1], R[1], acc);
+    acc = mfma4(LT[2], R[2], acc);
+    acc = mfma4(LT[3], R[3], acc);
+    return acc;
+}
+
+// Orders the LDS traffic of one wavefront (all lanes execute in lockstep, so
+// only the compiler and the memory counters need fencing).
+__device__ inline void wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// D-layout transpose through the wave's LDS scratch.
+__device__ inline f4 transpose16(f4 M, float *scr, int g, int c)
+{
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        scr[(4 * g + i) * kTrStride + c] = M[i];
+    wave_sync();
+    f4 r = *reinterpret_cast<const f4 *>(scr + c * kTrStride + 4 * g);
+    wave_sync();
+    return r;
+}
+
+// Per-token vector exchange: value x (held per lane column c, identical in
+// all four lane groups) returned at row positions 4g + i.
+__device__ inline f4 by_rows(float x, float *vec, int g, int c)
+{
+    if (g == 0)
+        vec[c] = x;
+    wave_sync();
+    f4 r = *reinterpret_cast<const f4 *>(vec + 4 * g);
+    wave_sync();
+    return r;
+}
+
+// ---- cross-lane operations (wave64; a "row" is 16 lanes) ------------------
+// DPP forms fuse into the consuming VALU instruction; swizzle and bpermute
+// go through the LDS crossbar without touching LDS memory.
+
+__device__ inline float dpp_xor1(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0xB1, 0xF, 0xF, false); }
+__device__ inline float dpp_xor2(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0x4E, 0xF, 0xF, false); }
+__device__ inline float dpp_ror4(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0x124, 0xF, 0xF, false); }
+// Rotating a 16-lane row by 8 is the exchange of lanes c and c ^ 8.
+__device__ inline float dpp_xor8(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0x128, 0xF, 0xF, false); }
+__device__ inline float swz_xor4(float x)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x101F));
+}
+
+// Exchange with lane ^ 16 (swizzle inside each 32-lane half) and with
+// lane ^ 32 (permute through the LDS crossbar; no LDS memory is used).
+__device__ inline float swz_xor16(float x)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x401F));
+}
+
+__device__ inline float perm_xor32(float x)
+{
+    const int addr = int((__lane_id() ^ 32u) << 2);
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(addr, __builtin_bit_cast(int, x)));
+}
+
+// Sum / max over the four lanes c, c^16, c^32, c^48 (the lane groups g).
+__device__ inline float sum_groups(float x)
+{
+    x += swz_xor16(x);
+    return x + perm_xor32(x);
+}
+
+__device__ inline float max_groups(float x)
+{
+    x = fmaxf(x, swz_xor16(x));
+    return fmaxf(x, perm_xor32(x));
+}
+
+// Sum / max over the 16 lanes of a row.
+__device__ inline float sum_row(float x)
+{
+    x += dpp_xor1(x);
+    x += dpp_xor2(x);
+    x += dpp_ror4(x);
+    return x + dpp_xor8(x);
+}
+
+__device__ inline float max_row(float x)
+{
+    x = fmaxf(x, dpp_xor1(x));
+    x = fmaxf(x, dpp_xor2(x));
+    x = fmaxf(x, dpp_ror4(x));
+    return fmaxf(x, dpp_xor8(x));
+}
+
+struct __attribute__((aligned(4))) U16B {
+    uint32_t w[4];
+};
+
+// Feature chunk of lane group g.  The contraction over features runs as
+// eight MFMA steps in which group g supplies the features in slots s = 0..7.
+// Slot s of group g holds feature f0(g) + s with f0(g) = min(8g, D - 8), so a
+// chunk never reaches past its row; slots whose feature belongs to a lower
+// group (f0 + s < 8g) are zeroed.  D (>= 8) is a compile-time constant, so
+// every load is in bounds and the masks are plain selects.
+template <int D>
+__device__ inline int chunk_start(int g) { return min(8 * g, D - 8); }
+
+template <int D>
+__device__ inline bool slot_valid(int g, int s) { return chunk_start<D>(g) + s >= 8 * g; }
+
+template <class E, int D>
+__device__ inline void load_chunk8(const typename E::T *row, int g, float *out)
+{
+    static_assert(D >= 8, "tiled kernel needs at least 8 features");
+    const int f0 = chunk_start<D>(g);
+    if constexpr (E::bytes == 4) {
+        const U16B a = *reinterpret_cast<const U16B *>(row + f0);
+        const U16B b = *reinterpret_cast<const U16B *>(row + f0 + 4);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            out[j] = slot_valid<D>(g, j) ? __uint_as_float(a.w[j]) : 0.f;
+            out[4 + j] = slot_valid<D>(g, 4 + j) ? __uint_as_float(b.w[j]) : 0.f;
+        }
+    } else {
+        const U16B a = *reinterpret_cast<const U16B *>(row + f0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            out[2 * j] = slot_valid<D>(g, 2 * j) ? __uint_as_float(a.w[j] << 16) : 0.f;
+            out[2 * j + 1] =
+                slot_valid<D>(g, 2 * j + 1) ? __uint_as_float(a.w[j] & 0xffff0000u) : 0.f;
+        }
+    }
+}
+
+}  // namespace tile
+}  // namespace nystra

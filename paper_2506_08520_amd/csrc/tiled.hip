@@ -1,181 +1,24 @@
 // MFMA-tiled PnP-Nystra kernel for small windows (N = 16, 32 or 64 tokens,
-// m <= 16 landmarks, d_h in {8, 16, 24, 30, 32}): one wavefront computes one (window, head)
-// unit entirely in registers, with every contraction on the fp32 matrix cores
-// (v_mfma_f32_16x16x4f32) and LDS used only for a few small exchanges.
-//
-// Register tile convention ("D-layout").  A 16x16 fp32 tile M lives in one
-// float4 per lane: lane (g = lane / 16, c = lane % 16) holds M[4g + i][c],
-// i = 0..3 -- the layout in which the MFMA returns its result.  Running the
-// 16-deep contraction as four MFMA steps in which lane group g supplies the
-// k-index 4g + s at step s, a D-layout tile can be fed back directly:
-//   mm16(LT, R) = L * R   when LT holds L^T and R holds R, both in D-layout.
-// So a product's result is immediately the right-hand operand of the next
-// product, and a matrix is usable as a left-hand operand once its transpose
-// is in D-layout.  The few transposes needed go through 1.25 KB of LDS.
+// m <= 16 landmarks, d_h in {8, 16, 24, 30, 32}): one wavefront computes one
+// (window, head) unit entirely in registers, with every contraction on the
+// fp32 matrix cores (v_mfma_f32_16x16x4f32, register tiles in the D-layout
+// of tile_common.hpp) and LDS used only for a few small exchanges.
 //
 // Contractions over the feature dimension (S_L, S_U, S_A) use eight MFMA
 // steps in which each lane group supplies a chunk of 8 consecutive features
 // of one token row, loaded straight from global memory in 16-byte pieces
 // (see load_chunk8).  All global loads are branch-free and in bounds, so the
 // compiler can keep every load of a unit in flight at once.
-#include "device_common.hpp"
 #include "internal.hpp"
+#include "tile_common.hpp"
 
 namespace nystra {
 namespace {
 
-typedef float f4 __attribute__((ext_vector_type(4)));
+using namespace tile;
 
 constexpr int kWavesPerBlock = 4;
-constexpr int kLdStride = 36;   // row stride (floats) of the landmark tiles in LDS
-constexpr int kTrStride = 20;   // row stride (floats) of the transpose scratch
 constexpr int kLdsPerWave = 2 * 16 * kLdStride + 16 * kTrStride + 64;
-
-__device__ inline f4 mfma4(float a, float b, f4 c)
-{
-    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-}
-
-// L * R for 16x16 tiles, LT = L^T and R in D-layout.
-__device__ inline f4 mm16(f4 LT, f4 R)
-{
-    f4 acc = {0.f, 0.f, 0.f, 0.f};
-    acc = mfma4(LT[0], R[0], acc);
-    acc = mfma4(LT[1], R[1], acc);
-    acc = mfma4(LT[2], R[2], acc);
-    acc = mfma4(LT[3], R[3], acc);
-    return acc;
-}
-
-// Orders the LDS traffic of one wavefront (all lanes execute in lockstep, so
-// only the compiler and the memory counters need fencing).
-__device__ inline void wave_sync()
-{
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-// D-layout transpose through the wave's LDS scratch.
-__device__ inline f4 transpose16(f4 M, float *scr, int g, int c)
-{
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-        scr[(4 * g + i) * kTrStride + c] = M[i];
-    wave_sync();
-    f4 r = *reinterpret_cast<const f4 *>(scr + c * kTrStride + 4 * g);
-    wave_sync();
-    return r;
-}
-
-// Per-token vector exchange: value x (held per lane column c, identical in
-// all four lane groups) returned at row positions 4g + i.
-__device__ inline f4 by_rows(float x, float *vec, int g, int c)
-{
-    if (g == 0)
-        vec[c] = x;
-    wave_sync();
-    f4 r = *reinterpret_cast<const f4 *>(vec + 4 * g);
-    wave_sync();
-    return r;
-}
-
-// ---- cross-lane operations (wave64; a "row" is 16 lanes) ------------------
-// DPP forms fuse into the consuming VALU instruction; swizzle and bpermute
-// go through the LDS crossbar without touching LDS memory.
-
-__device__ inline float dpp_xor1(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0xB1, 0xF, 0xF, false); }
-__device__ inline float dpp_xor2(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0x4E, 0xF, 0xF, false); }
-__device__ inline float dpp_ror4(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0x124, 0xF, 0xF, false); }
-// Rotating a 16-lane row by 8 is the exchange of lanes c and c ^ 8.
-__device__ inline float dpp_xor8(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0x128, 0xF, 0xF, false); }
-__device__ inline float swz_xor4(float x)
-{
-    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x101F));
-}
-
-// Exchange with lane ^ 16 (swizzle inside each 32-lane half) and with
-// lane ^ 32 (permute through the LDS crossbar; no LDS memory is used).
-__device__ inline float swz_xor16(float x)
-{
-    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x401F));
-}
-
-__device__ inline float perm_xor32(float x)
-{
-    const int addr = int((__lane_id() ^ 32u) << 2);
-    return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(addr, __builtin_bit_cast(int, x)));
-}
-
-// Sum / max over the four lanes c, c^16, c^32, c^48 (the lane groups g).
-__device__ inline float sum_groups(float x)
-{
-    x += swz_xor16(x);
-    return x + perm_xor32(x);
-}
-
-__device__ inline float max_groups(float x)
-{
-    x = fmaxf(x, swz_xor16(x));
-    return fmaxf(x, perm_xor32(x));
-}
-
-// Sum / max over the 16 lanes of a row.
-__device__ inline float sum_row(float x)
-{
-    x += dpp_xor1(x);
-    x += dpp_xor2(x);
-    x += dpp_ror4(x);
-    return x + dpp_xor8(x);
-}
-
-__device__ inline float max_row(float x)
-{
-    x = fmaxf(x, dpp_xor1(x));
-    x = fmaxf(x, dpp_xor2(x));
-    x = fmaxf(x, dpp_ror4(x));
-    return fmaxf(x, dpp_xor8(x));
-}
-
-struct __attribute__((aligned(4))) U16B {
-    uint32_t w[4];
-};
-
-// Feature chunk of lane group g.  The contraction over features runs as
-// eight MFMA steps in which group g supplies the features in slots s = 0..7.
-// Slot s of group g holds feature f0(g) + s with f0(g) = min(8g, D - 8), so a
-// chunk never reaches past its row; slots whose feature belongs to a lower
-// group (f0 + s < 8g) are zeroed.  D (>= 8) is a compile-time constant, so
-// every load is in bounds and the masks are plain selects.
-template <int D>
-__device__ inline int chunk_start(int g) { return min(8 * g, D - 8); }
-
-template <int D>
-__device__ inline bool slot_valid(int g, int s) { return chunk_start<D>(g) + s >= 8 * g; }
-
-template <class E, int D>
-__device__ inline void load_chunk8(const typename E::T *row, int g, float *out)
-{
-    static_assert(D >= 8, "tiled kernel needs at least 8 features");
-    const int f0 = chunk_start<D>(g);
-    if constexpr (E::bytes == 4) {
-        const U16B a = *reinterpret_cast<const U16B *>(row + f0);
-        const U16B b = *reinterpret_cast<const U16B *>(row + f0 + 4);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            out[j] = slot_valid<D>(g, j) ? __uint_as_float(a.w[j]) : 0.f;
-            out[4 + j] = slot_valid<D>(g, 4 + j) ? __uint_as_float(b.w[j]) : 0.f;
-        }
-    } else {
-        const U16B a = *reinterpret_cast<const U16B *>(row + f0);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            out[2 * j] = slot_valid<D>(g, 2 * j) ? __uint_as_float(a.w[j] << 16) : 0.f;
-            out[2 * j + 1] =
-                slot_valid<D>(g, 2 * j + 1) ? __uint_as_float(a.w[j] & 0xffff0000u) : 0.f;
-        }
-    }
-}
 
 // Step 1 for one input: writes the patch means of this wave's tokens to
 // bar[l][f] (LDS).  A patch is the set of tokens that agree with its base
@@ -468,9 +311,6 @@ void launch_small_d(const Problem &p, const SmallArgs &a, hipStream_t stream)
     }
 }
 
-// Head widths with a tiled instantiation.
-bool tiled_width(int d) { return d == 8 || d == 16 || d == 24 || d == 30 || d == 32; }
-
 template <class E>
 void launch_small_e(const Problem &p, const SmallArgs &a, hipStream_t stream)
 {
@@ -483,9 +323,7 @@ void launch_small_e(const Problem &p, const SmallArgs &a, hipStream_t stream)
     }
 }
 
-}  // namespace
-
-bool tiled_supported(const Problem &p)
+bool small_supported(const Problem &p)
 {
     const Geometry &g = p.geo;
     if (!(p.N == 16 || p.N == 32 || p.N == 64) || p.m > 16 || !tiled_width(p.d))
@@ -500,8 +338,14 @@ bool tiled_supported(const Problem &p)
     return true;
 }
 
+}  // namespace
+
+bool tiled_supported(const Problem &p) { return small_supported(p) || tiled_large_supported(p); }
+
 hipError_t launch_tiled_forward(const Problem &p, hipStream_t stream)
 {
+    if (!small_supported(p))
+        return launch_tiled_large(p, stream);
     SmallArgs a;
     a.units = p.units;
     a.m = p.m;

@@ -72,6 +72,12 @@ EDGE = [
     (7, 3, 16, 5, 4, 0),      # tiny window, many units
     (2, 2, 256, 30, 16, 0),   # fewer landmarks at N = 256
     (1, 3, 1024, 30, 32, 0),  # m = 32 at N = 1024
+    (2, 2, 64, 32, 32, 0),    # 1x2 patches, two landmark tiles at N = 64
+    (2, 1, 144, 24, 36, 0),   # 12x12 window, 6x6 grid of 2x2 patches (three tiles)
+    (1, 2, 4096, 32, 64, 0),  # largest window with four landmark tiles
+    (1, 2, 1024, 16, 64, 1),  # 1-D segments at N = 1024
+    (3, 2, 256, 8, 32, 1),    # 1-D segments, narrow head
+    (2, 2, 240, 24, 48, 1),   # three landmark tiles, 1-D segments
 ]
 
 
@@ -97,6 +103,17 @@ def test_iteration_counts(iters, variant):
     wl = W.CONFIGS["c1"]
     need_variant(wl.N, wl.d, wl.m, "f32", variant)
     q, k, v = W.generate(wl, "f32", n_windows=8)
+    ref = oracle.forward(q, k, v, wl.m, iters=iters)
+    got = run(q, k, v, wl.m, "f32", variant, iters=iters)
+    assert error(got, ref, "f32") <= TOL["f32"]
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("iters", [0, 1, 5, 8])
+def test_iteration_counts_large_window(iters, variant):
+    wl = W.CONFIGS["c4"]
+    need_variant(wl.N, wl.d, wl.m, "f32", variant)
+    q, k, v = W.generate(wl, "f32", n_windows=4)
     ref = oracle.forward(q, k, v, wl.m, iters=iters)
     got = run(q, k, v, wl.m, "f32", variant, iters=iters)
     assert error(got, ref, "f32") <= TOL["f32"]
