@@ -2,8 +2,17 @@
 // (window, head) unit, with the row maximum subtracted inside the softmax
 // (kept as a running maximum over key blocks).  This is the comparison
 // baseline for the Nystrom kernels.
-#include "device_common.hpp"
+//
+// exact_tiled_kernel (N % 32 == 0, d_h in the tiled widths): flash-style.
+// One wavefront owns 16 queries and walks the keys in blocks of 32.  Scores
+// are produced transposed, S^T = K Q^T, so each lane column is one query and
+// the running max / sum / rescale stay in the lane; the output is accumulated
+// transposed as well, O^T += V^T P^T.  fp32 inputs use the fp32 matrix cores;
+// bf16 inputs use v_mfma_f32_16x16x32_bf16 for both products with P rounded
+// to bf16 (V is staged transposed in LDS for the second product).
+// exact_rows_kernel: one thread per query row, any shape.
 #include "internal.hpp"
+#include "tile_common.hpp"
 
 namespace nystra {
 namespace {
@@ -77,9 +86,211 @@ exact_rows_kernel(const typename E::T *__restrict__ q, const typename E::T *__re
     }
 }
 
+using namespace tile;
+
+// Eight features of one row as raw bf16 pairs (slots outside the lane
+// group's chunk zeroed; see load_chunk8).  D is even, so invalid slots come
+// in whole 32-bit pairs.
+template <int D>
+__device__ inline U16B load_chunk8_raw(const uint16_t *row, int g)
+{
+    U16B u = *reinterpret_cast<const U16B *>(row + chunk_start<D>(g));
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        if (!slot_valid<D>(g, 2 * j))
+            u.w[j] = 0u;
+    return u;
+}
+
+__device__ inline bf8 as_bf8(const U16B &u) { return __builtin_bit_cast(bf8, u); }
+
+__device__ inline uint32_t pack_bf16(float lo, float hi)
+{
+    return uint32_t(f32_to_bf16(lo)) | (uint32_t(f32_to_bf16(hi)) << 16);
+}
+
+constexpr int kExactWaves = 4;
+
+template <class E, int D, bool BF>
+__global__ void __launch_bounds__(64 * kExactWaves)
+exact_tiled_kernel(const typename E::T *__restrict__ q, const typename E::T *__restrict__ k,
+                   const typename E::T *__restrict__ v, typename E::T *__restrict__ o, int N,
+                   float s2, int qblocks)
+{
+    extern __shared__ uint16_t vt[];   // bf16 only: V^T, [32 features][N + 8 keys]
+    constexpr int d = D;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int g = lane >> 4, c = lane & 15;
+    const int64_t unit = blockIdx.x / qblocks;
+    const int NT = N >> 4, pitch = N + 8;
+    const int qt = (blockIdx.x % qblocks) * kExactWaves + wave;   // query tile of this wave
+    const int64_t base = unit * int64_t(N) * d;
+    const typename E::T *qu = q + base, *ku = k + base, *vu = v + base;
+    typename E::T *ou = o + base;
+    constexpr bool bf = BF;   // bf16 inputs on the bf16 matrix cores
+
+    if constexpr (bf) {
+        for (int kt = wave; kt < NT; kt += kExactWaves) {
+            const U16B u = load_chunk8_raw<D>(
+                reinterpret_cast<const uint16_t *>(vu) + int64_t(16 * kt + c) * d, g);
+#pragma unroll
+            for (int s = 0; s < 8; ++s)
+                if (slot_valid<D>(g, s))
+                    vt[(chunk_start<D>(g) + s) * pitch + 16 * kt + c] =
+                        uint16_t(u.w[s >> 1] >> (16 * (s & 1)));
+        }
+        __syncthreads();
+    }
+    if (qt >= NT)
+        return;   // after the only block-level barrier
+
+    const int qrow = 16 * qt + c;
+    float qf[8];
+    U16B qraw;
+    if constexpr (bf)
+        qraw = load_chunk8_raw<D>(reinterpret_cast<const uint16_t *>(qu) + int64_t(qrow) * d, g);
+    else
+        load_chunk8<E, D>(qu + int64_t(qrow) * d, g, qf);
+
+    float mrun = -INFINITY, lrun = 0.f;
+    f4 OT[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};   // O^T[16ct+4g+i][query c]
+    for (int kb = 0; kb < NT; kb += 2) {
+        f4 S[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int key = 16 * (kb + h) + c;
+            f4 acc = {0.f, 0.f, 0.f, 0.f};
+            if constexpr (bf) {
+                const U16B kraw = load_chunk8_raw<D>(
+                    reinterpret_cast<const uint16_t *>(ku) + int64_t(key) * d, g);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(kraw), as_bf8(qraw), acc, 0,
+                                                             0, 0);
+            } else {
+                float kf[8];
+                load_chunk8<E, D>(ku + int64_t(key) * d, g, kf);
+#pragma unroll
+                for (int s = 0; s < 8; ++s)
+                    acc = mfma4(kf[s], qf[s], acc);
+            }
+            S[h] = acc;   // lane (g,c): S[query c][key 16(kb+h) + 4g + i]
+        }
+        float bmax = fmaxf(fmaxf(fmaxf(S[0][0], S[0][1]), fmaxf(S[0][2], S[0][3])),
+                           fmaxf(fmaxf(S[1][0], S[1][1]), fmaxf(S[1][2], S[1][3])));
+        const float mnew = fmaxf(mrun, s2 * max_groups(bmax));
+        const float sc = fast_exp2(mrun - mnew);
+        float psum = 0.f;
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                S[h][i] = fast_exp2(fmaf(s2, S[h][i], -mnew));
+                psum += S[h][i];
+            }
+        lrun = fmaf(lrun, sc, sum_groups(psum));
+        mrun = mnew;
+#pragma unroll
+        for (int ct = 0; ct < 2; ++ct) {
+            f4 upd;
+            if constexpr (bf) {
+                // A = V^T rows (feature 16ct+c), keys {4g..4g+3} of both tiles;
+                // B = P^T for the same keys.
+                const uint16_t *row = vt + (16 * ct + c) * pitch + 16 * kb + 4 * g;
+                const uint2 v0 = *reinterpret_cast<const uint2 *>(row);
+                const uint2 v1 = *reinterpret_cast<const uint2 *>(row + 16);
+                U16B a, b;
+                a.w[0] = v0.x; a.w[1] = v0.y; a.w[2] = v1.x; a.w[3] = v1.y;
+                b.w[0] = pack_bf16(S[0][0], S[0][1]);
+                b.w[1] = pack_bf16(S[0][2], S[0][3]);
+                b.w[2] = pack_bf16(S[1][0], S[1][1]);
+                b.w[3] = pack_bf16(S[1][2], S[1][3]);
+                upd = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(a), as_bf8(b),
+                                                             f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+            } else {
+                // LT = V tile in D-layout: V[key 16(kb+h) + 4g + i][feature 16ct + c].
+                const int f = 16 * ct + c;
+                upd = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    f4 vd;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float x = E::load(vu, int64_t(16 * (kb + h) + 4 * g + i) * d +
+                                                        min(f, d - 1));
+                        vd[i] = f < d ? x : 0.f;
+                    }
+                    upd += mm16(vd, S[h]);
+                }
+            }
+            OT[ct] = OT[ct] * sc + upd;
+        }
+    }
+    const float inv = __builtin_amdgcn_rcpf(lrun);
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int f = 16 * ct + 4 * g + i;
+            if (f < d)
+                E::store(ou, int64_t(qrow) * d + f, OT[ct][i] * inv);
+        }
+}
+
+// V^T of one unit in LDS for the bf16 path; larger windows run the fp32
+// matrix cores on the (exactly converted) bf16 inputs instead.
+constexpr size_t kExactLdsMax = 128 * 1024;
+
+template <class E, int D>
+void launch_exact_tiled(const Problem &p, hipStream_t stream)
+{
+    const int NT = p.N / 16;
+    const int qblocks = (NT + kExactWaves - 1) / kExactWaves;
+    const size_t lds = size_t(32) * (p.N + 8) * 2;
+    const auto *q = static_cast<const typename E::T *>(p.q);
+    const auto *k = static_cast<const typename E::T *>(p.k);
+    const auto *v = static_cast<const typename E::T *>(p.v);
+    auto *o = static_cast<typename E::T *>(p.o);
+    const dim3 grid(unsigned(p.units * qblocks)), block(64 * kExactWaves);
+    if (E::bytes == 2 && lds <= kExactLdsMax)
+        hipLaunchKernelGGL((exact_tiled_kernel<E, D, true>), grid, block, lds, stream, q, k, v,
+                           o, p.N, p.scale * kLog2e, qblocks);
+    else
+        hipLaunchKernelGGL((exact_tiled_kernel<E, D, false>), grid, block, 0, stream, q, k, v,
+                           o, p.N, p.scale * kLog2e, qblocks);
+}
+
+template <class E>
+void launch_exact_tiled_e(const Problem &p, hipStream_t stream)
+{
+    switch (p.d) {
+    case 8: launch_exact_tiled<E, 8>(p, stream); break;
+    case 16: launch_exact_tiled<E, 16>(p, stream); break;
+    case 24: launch_exact_tiled<E, 24>(p, stream); break;
+    case 30: launch_exact_tiled<E, 30>(p, stream); break;
+    default: launch_exact_tiled<E, 32>(p, stream); break;
+    }
+}
+
+bool exact_tiled_ok(const Problem &p)
+{
+    if (p.N % 32 != 0 || !tiled_width(p.d))
+        return false;
+    if (p.units * int64_t((p.N / 16 + kExactWaves - 1) / kExactWaves) > int64_t(INT32_MAX))
+        return false;
+    if (p.dtype == 1) {
+        const uintptr_t mis = uintptr_t(p.q) | uintptr_t(p.k) | uintptr_t(p.v);
+        if (mis % 4 != 0)
+            return false;
+    }
+    return true;
+}
+
 template <class E>
 hipError_t launch_exact_t(const Problem &p, hipStream_t stream)
 {
+    if (exact_tiled_ok(p)) {
+        launch_exact_tiled_e<E>(p, stream);
+        return hipGetLastError();
+    }
     const dim3 grid(unsigned(p.units), unsigned((p.N + kThreads - 1) / kThreads));
     hipLaunchKernelGGL(exact_rows_kernel<E>, grid, dim3(kThreads), 0, stream,
                        static_cast<const typename E::T *>(p.q),

@@ -38,6 +38,38 @@ __device__ inline f4 mm16(f4 LT, f4 R)
     return acc;
 }
 
+// acc + L * R, chaining the accumulator through the matrix core.
+__device__ inline f4 mm16_acc(f4 LT, f4 R, f4 acc)
+{
+    acc = mfma4(LT[0], R[0], acc);
+    acc = mfma4(LT[1], R[1], acc);
+    acc = mfma4(LT[2], R[2], acc);
+    acc = mfma4(LT[3], R[3], acc);
+    return acc;
+}
+
+// ---- bf16 matrix-core operands --------------------------------------------
+// v_mfma_f32_16x16x32_bf16: lane (g, c) supplies A[c][8g + j] and B[8g + j][c]
+// (j = 0..7) and receives D[4g + i][c].  An fp32 operand x is carried as two
+// bf16 terms, hi = bf16(x) and lo = bf16(x - hi), which keep ~16 bits.
+
+typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+
+__device__ inline f4 mfma_bf16(bf8 a, bf8 b, f4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ inline void split_bf16(const float (&x)[8], bf8 &hi, bf8 &lo)
+{
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const __bf16 h = (__bf16)x[j];
+        hi[j] = h;
+        lo[j] = (__bf16)(x[j] - (float)h);
+    }
+}
+
 // Orders the LDS traffic of one wavefront (all lanes execute in lockstep, so
 // only the compiler and the memory counters need fencing).
 __device__ inline void wave_sync()
@@ -166,6 +198,19 @@ __device__ inline void load_chunk8(const typename E::T *row, int g, float *out)
                 slot_valid<D>(g, 2 * j + 1) ? __uint_as_float(a.w[j] & 0xffff0000u) : 0.f;
         }
     }
+}
+
+// Eight features of one bf16 row as raw bits, in the slot layout of
+// load_chunk8 (D is even, so invalid slots come in whole 32-bit pairs).
+template <int D>
+__device__ inline bf8 load_chunk8_bf8(const uint16_t *row, int g)
+{
+    U16B u = *reinterpret_cast<const U16B *>(row + chunk_start<D>(g));
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        if (!slot_valid<D>(g, 2 * j))
+            u.w[j] = 0u;
+    return __builtin_bit_cast(bf8, u);
 }
 
 }  // namespace tile

@@ -82,7 +82,7 @@ __device__ inline void write_tile(float *B, int a, int b, f4 v, int g, int c)
         B[(16 * a + 4 * g + i) * P + 16 * b + c] = v[i];
 }
 
-template <class E, int MT, int D>
+template <class E, int MT, int D, bool BFM>
 __global__ void __launch_bounds__(64 * MT)
 tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__restrict__ k,
                    const typename E::T *__restrict__ v, typename E::T *__restrict__ o,
@@ -105,7 +105,8 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     const typename E::T *qu = q + base, *ku = k + base, *vu = v + base;
     typename E::T *ou = o + base;
 
-    // ---- Step 1: means of this landmark's patch (rows r0.., cols c0..).
+    // ---- Step 1: means of this landmark's patch (rows r0.., cols c0..),
+    // four patch tokens per step so their loads are in flight together.
     float qb[8], kbv[8];
 #pragma unroll
     for (int s = 0; s < 8; ++s)
@@ -113,18 +114,26 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     {
         const int le = lval ? l : m - 1;   // padding lanes read a valid patch, then drop it
         const int r0 = (le / a.gc) * a.pr, c0 = (le % a.gc) * a.pc;
-        for (int r = r0; r < r0 + a.pr; ++r)
-            for (int cc = c0; cc < c0 + a.pc; ++cc) {
-                float x[8], y[8];
-                const int64_t t = int64_t(r) * a.cols + cc;
-                load_chunk8<E, D>(qu + t * d, g, x);
-                load_chunk8<E, D>(ku + t * d, g, y);
+        const int npatch = a.pr * a.pc;
+        for (int j0 = 0; j0 < npatch; j0 += 4) {
+            float x[4][8], y[4][8];
 #pragma unroll
-                for (int s = 0; s < 8; ++s) {
-                    qb[s] += x[s];
-                    kbv[s] += y[s];
-                }
+            for (int u = 0; u < 4; ++u) {
+                const int j = min(j0 + u, npatch - 1);
+                const int64_t t = int64_t(r0 + j / a.pc) * a.cols + c0 + j % a.pc;
+                load_chunk8<E, D>(qu + t * d, g, x[u]);
+                load_chunk8<E, D>(ku + t * d, g, y[u]);
             }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (j0 + u < npatch) {
+#pragma unroll
+                    for (int s = 0; s < 8; ++s) {
+                        qb[s] += x[u][s];
+                        kbv[s] += y[u][s];
+                    }
+                }
+        }
         const float sc = lval ? a.inv_patch : 0.f;
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
@@ -137,21 +146,41 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         if (slot_valid<D>(g, s))
             kbar[l * kTS + chunk_start<D>(g) + s] = kbv[s];
 
-    // ---- Step 3, G_U side, pass 1: m_U of this landmark over all N keys.
-    float mx = -INFINITY;
-    {
-        float kn[8];
-        load_chunk8<E, D>(ku + int64_t(c) * d, g, kn);
-        for (int tt = 0; tt < NT; ++tt) {
-            float kr[8];
-#pragma unroll
-            for (int s = 0; s < 8; ++s)
-                kr[s] = kn[s];
-            load_chunk8<E, D>(ku + int64_t(16 * min(tt + 1, NT - 1) + c) * d, g, kn);
-            f4 acc = {0.f, 0.f, 0.f, 0.f};
+    // ---- Step 3, G_U side, pass 1: m_U of this landmark over all N keys,
+    // kGroup key tiles per step (a repeated last tile leaves the max unchanged).
+    constexpr int kGroup = 4;
+    const uint16_t *ku16 = reinterpret_cast<const uint16_t *>(ku);
+    bf8 qbh, qbl;   // bf16 path: Qbar row as hi + lo terms
+    if constexpr (BFM)
+        split_bf16(qb, qbh, qbl);
+    // S_U^T tile for key tile tt: lane (g,c) gets S_U[landmark l][key 16tt + 4g + i].
+    auto su_tile = [&](int tt, const float *kr, const bf8 &kraw) {
+        f4 acc = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (BFM) {
+            acc = mfma_bf16(kraw, qbh, acc);
+            acc = mfma_bf16(kraw, qbl, acc);
+        } else {
 #pragma unroll
             for (int s = 0; s < 8; ++s)
                 acc = mfma4(kr[s], qb[s], acc);
+        }
+        return acc;
+    };
+    float mx = -INFINITY;
+    for (int t0 = 0; t0 < NT; t0 += kGroup) {
+        float kr[kGroup][8];
+        bf8 kw[kGroup];
+#pragma unroll
+        for (int u = 0; u < kGroup; ++u) {
+            const int64_t row = int64_t(16 * min(t0 + u, NT - 1) + c) * d;
+            if constexpr (BFM)
+                kw[u] = load_chunk8_bf8<D>(ku16 + row, g);
+            else
+                load_chunk8<E, D>(ku + row, g, kr[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < kGroup; ++u) {
+            const f4 acc = su_tile(t0 + u, kr[u], kw[u]);
             mx = fmaxf(mx, fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3])));
         }
     }
@@ -161,46 +190,83 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     // T[ct] lane (g,c): T[landmark 16lt+4g+i][feature 16ct+c].
     f4 T[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
     float tden = 0.f;
-    {
-        float kn[8], vn[2][4];
-        auto load_tile = [&](int tt, float *kx, float (*vx)[4]) {
-            load_chunk8<E, D>(ku + int64_t(16 * tt + c) * d, g, kx);
+    const uint16_t *vu16 = reinterpret_cast<const uint16_t *>(vu);
+    for (int t0 = 0; t0 < NT; t0 += kGroup) {
+        float kr[kGroup][8], vr[kGroup][2][4];
+        bf8 kw[kGroup];
+        uint16_t vh[kGroup][2][4];
+#pragma unroll
+        for (int u = 0; u < kGroup; ++u) {
+            const int tt = min(t0 + u, NT - 1);
+            const int64_t row = int64_t(16 * tt + c) * d;
+            if constexpr (BFM)
+                kw[u] = load_chunk8_bf8<D>(ku16 + row, g);
+            else
+                load_chunk8<E, D>(ku + row, g, kr[u]);
 #pragma unroll
             for (int ct = 0; ct < 2; ++ct) {
                 const int f = 16 * ct + c;
 #pragma unroll
                 for (int s = 0; s < 4; ++s) {
-                    const float x = E::load(vu, int64_t(16 * tt + 4 * g + s) * d + min(f, d - 1));
-                    vx[ct][s] = f < d ? x : 0.f;
+                    const int64_t idx = int64_t(16 * tt + 4 * g + s) * d + min(f, d - 1);
+                    if constexpr (BFM) {
+                        const uint16_t x = vu16[idx];
+                        vh[u][ct][s] = f < d ? x : uint16_t(0);
+                    } else {
+                        const float x = E::load(vu, idx);
+                        vr[u][ct][s] = f < d ? x : 0.f;
+                    }
                 }
             }
-        };
-        load_tile(0, kn, vn);
-        for (int tt = 0; tt < NT; ++tt) {
-            float kr[8], vr[2][4];
+        }
+        if constexpr (BFM) {
+            // Key tiles in pairs: the bf16 product contracts 32 keys, lane group g
+            // supplying keys 4g..4g+3 of both tiles.  N % 32 == 0 on this path.
 #pragma unroll
-            for (int s = 0; s < 8; ++s)
-                kr[s] = kn[s];
+            for (int u = 0; u < kGroup; u += 2) {
+                if (t0 + u >= NT)
+                    break;   // uniform
+                float gk[8];
 #pragma unroll
-            for (int ct = 0; ct < 2; ++ct)
+                for (int h = 0; h < 2; ++h) {
+                    const f4 acc = su_tile(t0 + u + h, kr[u + h], kw[u + h]);
 #pragma unroll
-                for (int s = 0; s < 4; ++s)
-                    vr[ct][s] = vn[ct][s];
-            load_tile(min(tt + 1, NT - 1), kn, vn);
-            f4 acc = {0.f, 0.f, 0.f, 0.f};
+                    for (int i = 0; i < 4; ++i) {
+                        gk[4 * h + i] = lval ? fast_exp2(fmaf(a.s2, acc[i], -mu)) : 0.f;
+                        tden += gk[4 * h + i];
+                    }
+                }
+                bf8 gh, gl;
+                split_bf16(gk, gh, gl);
 #pragma unroll
-            for (int s = 0; s < 8; ++s)
-                acc = mfma4(kr[s], qb[s], acc);
+                for (int ct = 0; ct < 2; ++ct) {
+                    U16B vb;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                acc[i] = lval ? fast_exp2(fmaf(a.s2, acc[i], -mu)) : 0.f;
-                tden += acc[i];
+                    for (int j = 0; j < 4; ++j)
+                        vb.w[j] = uint32_t(vh[u + (j >> 1)][ct][2 * (j & 1)]) |
+                                  (uint32_t(vh[u + (j >> 1)][ct][2 * (j & 1) + 1]) << 16);
+                    const bf8 vv = __builtin_bit_cast(bf8, vb);
+                    T[ct] = mfma_bf16(gh, vv, T[ct]);
+                    T[ct] = mfma_bf16(gl, vv, T[ct]);
+                }
             }
+        } else {
 #pragma unroll
-            for (int ct = 0; ct < 2; ++ct)
+            for (int u = 0; u < kGroup; ++u) {
+                if (t0 + u >= NT)
+                    break;   // uniform
+                f4 acc = su_tile(t0 + u, kr[u], kw[u]);
 #pragma unroll
-                for (int s = 0; s < 4; ++s)
-                    T[ct] = mfma4(acc[s], vr[ct][s], T[ct]);
+                for (int i = 0; i < 4; ++i) {
+                    acc[i] = lval ? fast_exp2(fmaf(a.s2, acc[i], -mu)) : 0.f;
+                    tden += acc[i];
+                }
+#pragma unroll
+                for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+                    for (int s = 0; s < 4; ++s)
+                        T[ct] = mfma4(acc[s], vr[u][ct][s], T[ct]);
+            }
         }
     }
     tden = sum_groups(tden);   // T_D of landmark l
@@ -306,7 +372,7 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             f4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int kk = 0; kk < MT; ++kk)
-                acc += mm16(XLT[kk], read_r<P>(Ya, kk, j, g, c));
+                acc = mm16_acc(XLT[kk], read_r<P>(Ya, kk, j, g, c), acc);
             Y[j] = (j == lt ? eye * 15.f : f4{0.f, 0.f, 0.f, 0.f}) - acc;
         }
 #pragma unroll
@@ -318,7 +384,7 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             f4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int kk = 0; kk < MT; ++kk)
-                acc += mm16(XLT[kk], read_r<P>(Yb, kk, j, g, c));
+                acc = mm16_acc(XLT[kk], read_r<P>(Yb, kk, j, g, c), acc);
             Y[j] = (j == lt ? eye * 13.f : f4{0.f, 0.f, 0.f, 0.f}) - acc;
         }
 #pragma unroll
@@ -331,7 +397,7 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             f4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int kk = 0; kk < MT; ++kk)
-                acc += mm16(ZLT[kk], read_r<P>(Ya, kk, j, g, c));
+                acc = mm16_acc(ZLT[kk], read_r<P>(Ya, kk, j, g, c), acc);
             Zn[j] = acc * 0.25f;
         }
 #pragma unroll
@@ -358,7 +424,7 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         f4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < MT; ++kk)
-            acc += mm16(ZLT[kk], read_r<kTS>(Tb, kk, ct, g, c));
+            acc = mm16_acc(ZLT[kk], read_r<kTS>(Tb, kk, ct, g, c), acc);
         Wt[ct] = acc;
     }
     float wden = 0.f;
@@ -377,6 +443,7 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     __syncthreads();
 
     // ---- Steps 3 (G_L side), 6 and 7 over this wave's token tiles.
+    constexpr int MP = (MT + 1) / 2;   // landmark tile pairs (bf16 path)
     f4 WR[MT][2], wdv[MT];
     float kb[MT][8];
 #pragma unroll
@@ -389,70 +456,137 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             kb[kk][s] = slot_valid<D>(g, s)
                             ? kbar[(16 * kk + c) * kTS + chunk_start<D>(g) + s] : 0.f;
     }
-    float qn[8];
-    load_chunk8<E, D>(qu + int64_t(16 * min(lt, NT - 1) + c) * d, g, qn);
-    for (int tt = lt; tt < NT; tt += MT) {
-        float qr[8];
-#pragma unroll
-        for (int s = 0; s < 8; ++s)
-            qr[s] = qn[s];
-        load_chunk8<E, D>(qu + int64_t(16 * min(tt + MT, NT - 1) + c) * d, g, qn);
-        f4 glT[MT];   // lane (g,c): G_L^n[token 16tt+c][landmark 16kk+4g+i]
-        float ml = -INFINITY;
-#pragma unroll
-        for (int kk = 0; kk < MT; ++kk) {
-            f4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int s = 0; s < 8; ++s)
-                acc = mfma4(kb[kk][s], qr[s], acc);
-            glT[kk] = acc;
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                if (16 * kk + 4 * g + i < m)
-                    ml = fmaxf(ml, acc[i]);
-        }
-        ml = a.s2 * max_groups(ml);
-        float od = 0.f;
+    // bf16 path: Kbar rows and W as hi + lo terms.  W pairs landmark tiles
+    // (2kp, 2kp+1): lane group g supplies landmarks 4g..4g+3 of both.
+    bf8 kbh[MT], kbl[MT], wh[MP][2], wl[MP][2];
+    if constexpr (BFM) {
 #pragma unroll
         for (int kk = 0; kk < MT; ++kk)
+            split_bf16(kb[kk], kbh[kk], kbl[kk]);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float e = (16 * kk + 4 * g + i < m) ? fast_exp2(fmaf(a.s2, glT[kk][i], -ml))
-                                                          : 0.f;
-                glT[kk][i] = e;
-                od = fmaf(e, wdv[kk][i], od);
+        for (int kp = 0; kp < MP; ++kp)
+#pragma unroll
+            for (int ct = 0; ct < 2; ++ct) {
+                float w8[8];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    w8[i] = WR[2 * kp][ct][i];
+                    w8[4 + i] = (2 * kp + 1 < MT) ? WR[(2 * kp + 1) % MT][ct][i] : 0.f;
+                }
+                split_bf16(w8, wh[kp][ct], wl[kp][ct]);
             }
-        od = sum_groups(od);
-        const f4 odr = by_rows(od, vec, g, c);   // O_D[16tt + 4g + i]
-        f4 rcp;
+    }
+    const uint16_t *qu16 = reinterpret_cast<const uint16_t *>(qu);
+    // Token tiles of this wave: lt, lt + MT, ...; the Q rows of kQGroup tiles
+    // are loaded together.
+    constexpr int kQGroup = 2;
+    for (int t0 = lt; t0 < NT; t0 += kQGroup * MT) {
+        float qg[kQGroup][8];
+        bf8 qw[kQGroup];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            rcp[i] = __builtin_amdgcn_rcpf(odr[i]);
+        for (int u = 0; u < kQGroup; ++u) {
+            const int64_t row = int64_t(16 * min(t0 + u * MT, NT - 1) + c) * d;
+            if constexpr (BFM)
+                qw[u] = load_chunk8_bf8<D>(qu16 + row, g);
+            else
+                load_chunk8<E, D>(qu + row, g, qg[u]);
+        }
 #pragma unroll
-        for (int ct = 0; ct < 2; ++ct) {
-            f4 on = {0.f, 0.f, 0.f, 0.f};
+        for (int u = 0; u < kQGroup; ++u) {
+            const int tt = t0 + u * MT;
+            if (tt >= NT)
+                break;   // uniform
+            f4 glT[MT];   // lane (g,c): G_L^n[token 16tt+c][landmark 16kk+4g+i]
+            float ml = -INFINITY;
 #pragma unroll
-            for (int kk = 0; kk < MT; ++kk)
-                on += mm16(glT[kk], WR[kk][ct]);
-            const int f = 16 * ct + c;
-            if (f < d) {
+            for (int kk = 0; kk < MT; ++kk) {
+                f4 acc = {0.f, 0.f, 0.f, 0.f};
+                if constexpr (BFM) {
+                    acc = mfma_bf16(kbh[kk], qw[u], acc);
+                    acc = mfma_bf16(kbl[kk], qw[u], acc);
+                } else {
+#pragma unroll
+                    for (int s = 0; s < 8; ++s)
+                        acc = mfma4(kb[kk][s], qg[u][s], acc);
+                }
+                glT[kk] = acc;
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    E::store(ou, int64_t(16 * tt + 4 * g + i) * d + f, on[i] * rcp[i]);
+                    if (16 * kk + 4 * g + i < m)
+                        ml = fmaxf(ml, acc[i]);
+            }
+            ml = a.s2 * max_groups(ml);
+            float od = 0.f;
+#pragma unroll
+            for (int kk = 0; kk < MT; ++kk)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float e = (16 * kk + 4 * g + i < m)
+                                        ? fast_exp2(fmaf(a.s2, glT[kk][i], -ml)) : 0.f;
+                    glT[kk][i] = e;
+                    od = fmaf(e, wdv[kk][i], od);
+                }
+            od = sum_groups(od);
+            const f4 odr = by_rows(od, vec, g, c);   // O_D[16tt + 4g + i]
+            f4 rcp;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                rcp[i] = __builtin_amdgcn_rcpf(odr[i]);
+            bf8 gh[MP], gl[MP];
+            if constexpr (BFM) {
+#pragma unroll
+                for (int kp = 0; kp < MP; ++kp) {
+                    float g8[8];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        g8[i] = glT[2 * kp][i];
+                        g8[4 + i] = (2 * kp + 1 < MT) ? glT[(2 * kp + 1) % MT][i] : 0.f;
+                    }
+                    split_bf16(g8, gh[kp], gl[kp]);
+                }
+            }
+#pragma unroll
+            for (int ct = 0; ct < 2; ++ct) {
+                f4 on = {0.f, 0.f, 0.f, 0.f};
+                if constexpr (BFM) {
+#pragma unroll
+                    for (int kp = 0; kp < MP; ++kp) {
+                        on = mfma_bf16(gh[kp], wh[kp][ct], on);
+                        on = mfma_bf16(gh[kp], wl[kp][ct], on);
+                        on = mfma_bf16(gl[kp], wh[kp][ct], on);
+                    }
+                } else {
+#pragma unroll
+                    for (int kk = 0; kk < MT; ++kk)
+                        on = mm16_acc(glT[kk], WR[kk][ct], on);
+                }
+                const int f = 16 * ct + c;
+                if (f < d) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        E::store(ou, int64_t(16 * tt + 4 * g + i) * d + f, on[i] * rcp[i]);
+                }
             }
         }
     }
 }
 
+// bf16 inputs with N % 32 == 0 take the bf16 matrix-core path.
 template <class E, int MT, int D>
 void launch_large(const Problem &p, const LargeArgs &a, hipStream_t stream)
 {
     const size_t lds = size_t(LargeLds<MT>::total) * sizeof(float);
-    hipLaunchKernelGGL((tiled_large_kernel<E, MT, D>), dim3(unsigned(p.units)), dim3(64 * MT),
-                       lds, stream, static_cast<const typename E::T *>(p.q),
-                       static_cast<const typename E::T *>(p.k),
-                       static_cast<const typename E::T *>(p.v),
-                       static_cast<typename E::T *>(p.o), a);
+    const auto *q = static_cast<const typename E::T *>(p.q);
+    const auto *k = static_cast<const typename E::T *>(p.k);
+    const auto *v = static_cast<const typename E::T *>(p.v);
+    auto *o = static_cast<typename E::T *>(p.o);
+    const dim3 grid(unsigned(p.units)), block(64 * MT);
+    if (E::bytes == 2 && p.N % 32 == 0)
+        hipLaunchKernelGGL((tiled_large_kernel<E, MT, D, E::bytes == 2>), grid, block, lds,
+                           stream, q, k, v, o, a);
+    else
+        hipLaunchKernelGGL((tiled_large_kernel<E, MT, D, false>), grid, block, lds, stream, q,
+                           k, v, o, a);
 }
 
 template <class E, int D>
