@@ -213,5 +213,24 @@ __device__ inline bf8 load_chunk8_bf8(const uint16_t *row, int g)
     return __builtin_bit_cast(bf8, u);
 }
 
+__device__ inline void unpack_bf8(bf8 v, float *out)
+{
+    const U16B u = __builtin_bit_cast(U16B, v);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        out[2 * j] = __uint_as_float(u.w[j] << 16);
+        out[2 * j + 1] = __uint_as_float(u.w[j] & 0xffff0000u);
+    }
+}
+
+__device__ inline bf8 pack_bf8(const uint16_t (&x)[8])
+{
+    U16B u;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        u.w[j] = uint32_t(x[2 * j]) | (uint32_t(x[2 * j + 1]) << 16);
+    return __builtin_bit_cast(bf8, u);
+}
+
 }  // namespace tile
 }  // namespace nystra

@@ -81,7 +81,7 @@ struct SmallArgs {
     int lg_cols, lg_pr, lg_pc, lg_gc, free_bits;   // pooling grid (log2 sizes)
 };
 
-template <class E, int NT, int D>
+template <class E, int NT, int D, bool BFM>
 __global__ void __launch_bounds__(64 * kWavesPerBlock)
 tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__restrict__ k,
                    const typename E::T *__restrict__ v, typename E::T *__restrict__ o,
@@ -106,16 +106,25 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     typename E::T *ou = o + base;
 
     // ---- Step 1: load token rows (features 8g..8g+7 of token 16tt+c) and pool.
+    // bf16 inputs (BFM) keep their raw bits for the bf16 matrix cores.
     float qr[NT][8], kr[NT][8];
+    bf8 qw[NT], kw[NT];
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt) {
-        load_chunk8<E, D>(qu + int64_t(16 * tt + c) * d, g, qr[tt]);
-        load_chunk8<E, D>(ku + int64_t(16 * tt + c) * d, g, kr[tt]);
+        const int64_t row = int64_t(16 * tt + c) * d;
+        if constexpr (BFM) {
+            qw[tt] = load_chunk8_bf8<D>(reinterpret_cast<const uint16_t *>(qu) + row, g);
+            kw[tt] = load_chunk8_bf8<D>(reinterpret_cast<const uint16_t *>(ku) + row, g);
+        } else {
+            load_chunk8<E, D>(qu + row, g, qr[tt]);
+            load_chunk8<E, D>(ku + row, g, kr[tt]);
+        }
     }
     // V in the right-hand operand layout of T = G_U^n V: vr[tt][ct][s] =
     // V[token 16tt+4g+s][feature 16ct+c] (zero past d).  Issued together with
     // Q and K so that all of the unit's loads are in flight at once.
     float vr[NT][2][4];
+    uint16_t vh[NT][2][4];
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
@@ -123,11 +132,24 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             const int f = 16 * ct + c;
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
-                const float x = E::load(vu, int64_t(16 * tt + 4 * g + s) * d + min(f, d - 1));
-                vr[tt][ct][s] = f < d ? x : 0.f;
+                const int64_t idx = int64_t(16 * tt + 4 * g + s) * d + min(f, d - 1);
+                if constexpr (BFM) {
+                    const uint16_t x = reinterpret_cast<const uint16_t *>(vu)[idx];
+                    vh[tt][ct][s] = f < d ? x : uint16_t(0);
+                } else {
+                    const float x = E::load(vu, idx);
+                    vr[tt][ct][s] = f < d ? x : 0.f;
+                }
             }
         }
     __builtin_amdgcn_sched_barrier(0);
+    if constexpr (BFM) {
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt) {
+            unpack_bf8(qw[tt], qr[tt]);
+            unpack_bf8(kw[tt], kr[tt]);
+        }
+    }
     // Landmark rows m..15 are padding: zero them so they contribute nothing.
     for (int idx = lane; idx < (16 - m) * 32; idx += 64) {
         const int r = m + idx / 32, f = idx % 32;
@@ -147,6 +169,11 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         kb_a[s] = ok ? kbar[c * kLdStride + f] : 0.f;
         qb_b[s] = ok ? qbar[c * kLdStride + f] : 0.f;
     }
+    bf8 kbh, kbl, qbh, qbl;   // bf16 path: landmark rows as hi + lo terms
+    if constexpr (BFM) {
+        split_bf16(kb_a, kbh, kbl);
+        split_bf16(qb_b, qbh, qbl);
+    }
 
     // ---- Step 3, G_L side: S_L^T tiles, row max over landmarks, G_L^n.
     // glT[tt] lane (g,c): G_L^n[token 16tt+c][landmark 4g+i].
@@ -154,9 +181,14 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt) {
         f4 acc = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (BFM) {
+            acc = mfma_bf16(kbh, qw[tt], acc);
+            acc = mfma_bf16(kbl, qw[tt], acc);
+        } else {
 #pragma unroll
-        for (int s = 0; s < 8; ++s)
-            acc = mfma4(kb_a[s], qr[tt][s], acc);
+            for (int s = 0; s < 8; ++s)
+                acc = mfma4(kb_a[s], qr[tt][s], acc);
+        }
         float mx = -INFINITY;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -175,9 +207,14 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt) {
         f4 acc = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (BFM) {
+            acc = mfma_bf16(kw[tt], qbh, acc);
+            acc = mfma_bf16(kw[tt], qbl, acc);
+        } else {
 #pragma unroll
-        for (int s = 0; s < 8; ++s)
-            acc = mfma4(kr[tt][s], qb_b[s], acc);
+            for (int s = 0; s < 8; ++s)
+                acc = mfma4(kr[tt][s], qb_b[s], acc);
+        }
         guT[tt] = acc;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -198,15 +235,44 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     // ---- Step 6, first product: T = G_U^n V  (16 landmarks x 32 features).
     // T[ct] lane (g,c): T[landmark 4g+i][feature 16ct+c].
     f4 T[2];
+    if constexpr (BFM) {
+        // token tiles in pairs: lane group g supplies tokens 4g..4g+3 of both
+        T[0] = T[1] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int ct = 0; ct < 2; ++ct) {
-        f4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int tp = 0; tp < (NT + 1) / 2; ++tp) {
+            const int t1 = 2 * tp + 1;
+            float g8[8];
 #pragma unroll
-        for (int tt = 0; tt < NT; ++tt)
+            for (int i = 0; i < 4; ++i) {
+                g8[i] = guT[2 * tp][i];
+                g8[4 + i] = t1 < NT ? guT[t1 % NT][i] : 0.f;
+            }
+            bf8 gh, gl;
+            split_bf16(g8, gh, gl);
 #pragma unroll
-            for (int s = 0; s < 4; ++s)
-                acc = mfma4(guT[tt][s], vr[tt][ct][s], acc);
-        T[ct] = acc;
+            for (int ct = 0; ct < 2; ++ct) {
+                uint16_t v8[8];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    v8[i] = vh[2 * tp][ct][i];
+                    v8[4 + i] = t1 < NT ? vh[t1 % NT][ct][i] : uint16_t(0);
+                }
+                const bf8 vv = pack_bf8(v8);
+                T[ct] = mfma_bf16(gh, vv, T[ct]);
+                T[ct] = mfma_bf16(gl, vv, T[ct]);
+            }
+        }
+    } else {
+#pragma unroll
+        for (int ct = 0; ct < 2; ++ct) {
+            f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+                for (int s = 0; s < 4; ++s)
+                    acc = mfma4(guT[tt][s], vr[tt][ct][s], acc);
+            T[ct] = acc;
+        }
     }
 
     // ---- Step 2: G_A^n (rows scaled by m_U).  AT lane (g,c): A[c][4g+i].
@@ -256,6 +322,15 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         wden = sum_groups(ZT[0] * td[0] + ZT[1] * td[1] + ZT[2] * td[2] + ZT[3] * td[3]);
     }
     const f4 wd = by_rows(wden, vec, g, c);                        // W_D[4g+i]
+    // bf16 path: W as hi + lo terms (landmark slots 4g..4g+3, upper half zero).
+    bf8 wh[2], wl[2];
+    if constexpr (BFM) {
+#pragma unroll
+        for (int ct = 0; ct < 2; ++ct) {
+            const float w8[8] = {Wt[ct][0], Wt[ct][1], Wt[ct][2], Wt[ct][3], 0.f, 0.f, 0.f, 0.f};
+            split_bf16(w8, wh[ct], wl[ct]);
+        }
+    }
 
     // ---- Steps 3 (G_L side), 6 and 7 per token tile: O = G_L^n W / O_D.
 #pragma unroll
@@ -267,9 +342,21 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 #pragma unroll
         for (int i = 0; i < 4; ++i)
             rcp[i] = __builtin_amdgcn_rcpf(odr[i]);
+        bf8 gh, gl;
+        if constexpr (BFM) {
+            const float g8[8] = {glT[tt][0], glT[tt][1], glT[tt][2], glT[tt][3], 0.f, 0.f, 0.f, 0.f};
+            split_bf16(g8, gh, gl);
+        }
 #pragma unroll
         for (int ct = 0; ct < 2; ++ct) {
-            const f4 on = mm16(glT[tt], Wt[ct]);
+            f4 on;
+            if constexpr (BFM) {
+                on = mfma_bf16(gh, wh[ct], f4{0.f, 0.f, 0.f, 0.f});
+                on = mfma_bf16(gh, wl[ct], on);
+                on = mfma_bf16(gl, wh[ct], on);
+            } else {
+                on = mm16(glT[tt], Wt[ct]);
+            }
             const int f = 16 * ct + c;
             if (f < d) {
 #pragma unroll
@@ -294,7 +381,8 @@ template <class E, int NT, int D>
 void launch_small(const Problem &p, const SmallArgs &a, hipStream_t stream)
 {
     const unsigned blocks = unsigned((p.units + kWavesPerBlock - 1) / kWavesPerBlock);
-    hipLaunchKernelGGL((tiled_small_kernel<E, NT, D>), dim3(blocks), dim3(64 * kWavesPerBlock),
+    hipLaunchKernelGGL((tiled_small_kernel<E, NT, D, E::bytes == 2>), dim3(blocks),
+                       dim3(64 * kWavesPerBlock),
                        0, stream, static_cast<const typename E::T *>(p.q),
                        static_cast<const typename E::T *>(p.k),
                        static_cast<const typename E::T *>(p.v),

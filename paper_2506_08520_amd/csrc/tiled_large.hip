@@ -40,16 +40,18 @@ struct LargeArgs {
 template <int MT>
 struct LargeLds {
     static constexpr int M = 16 * MT;
-    static constexpr int P = M + 4;   // pitch of the m x m matrices
+    static constexpr int P = M + 4;    // pitch (floats) of fp32 m x m matrices
+    static constexpr int PB = M + 8;   // pitch (bf16 elements) of transposed bf16 matrices
+    static constexpr int RS = M * PB;  // one matrix region (floats): fp32 [M][P] or bf16 hi+lo
     static constexpr int kbar = 0;
     static constexpr int colpart = kbar + M * kTS;      // [MT][M] column-sum partials
     static constexpr int rowmax = colpart + MT * M;     // [MT] row-sum maxima (padded)
     static constexpr int zb = rowmax + 4;
-    static constexpr int ya = zb + M * P;
-    static constexpr int yb = ya + M * P;               // also the own-row X scratch
-    static constexpr int vec = yb + M * P;              // [MT][64]
+    static constexpr int ya = zb + RS;
+    static constexpr int yb = ya + RS;                  // also the own-row transpose scratch
+    static constexpr int vec = yb + RS;                 // [MT][64]
     static constexpr int tab_len = M * kTS + M;         // table + its denominator column
-    static constexpr bool tab_in_y = tab_len <= M * P;  // T in ya, W in yb after the iteration
+    static constexpr bool tab_in_y = tab_len <= RS;     // T in ya, W in yb after the iteration
     static constexpr int tb = tab_in_y ? ya : vec + MT * 64;
     static constexpr int wb = tab_in_y ? yb : tb + tab_len;
     static constexpr int total = tab_in_y ? vec + MT * 64 : wb + tab_len;
@@ -80,6 +82,56 @@ __device__ inline void write_tile(float *B, int a, int b, f4 v, int g, int c)
 #pragma unroll
     for (int i = 0; i < 4; ++i)
         B[(16 * a + 4 * g + i) * P + 16 * b + c] = v[i];
+}
+
+// bf16 copies of an m x m matrix for the bf16 matrix cores: hi and lo terms,
+// each stored transposed ([column][row], pitch PB) so that the right-hand
+// operand of a 32-deep product -- rows 32kp + 4g .. +3 and 32kp + 16 + 4g .. +3
+// of one column -- is two 8-byte reads.  The writer splits once.
+template <int M, int PB>
+__device__ inline void publish_bf(uint16_t *reg, int a, int b, f4 v, int g, int c)
+{
+    uint32_t h[2], l[2];
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+        const __bf16 h0 = (__bf16)v[2 * p], h1 = (__bf16)v[2 * p + 1];
+        const __bf16 l0 = (__bf16)(v[2 * p] - (float)h0), l1 = (__bf16)(v[2 * p + 1] - (float)h1);
+        h[p] = uint32_t(__builtin_bit_cast(uint16_t, h0)) |
+               (uint32_t(__builtin_bit_cast(uint16_t, h1)) << 16);
+        l[p] = uint32_t(__builtin_bit_cast(uint16_t, l0)) |
+               (uint32_t(__builtin_bit_cast(uint16_t, l1)) << 16);
+    }
+    uint16_t *hp = reg + (16 * b + c) * PB + 16 * a + 4 * g;
+    *reinterpret_cast<uint2 *>(hp) = make_uint2(h[0], h[1]);
+    *reinterpret_cast<uint2 *>(hp + M * PB) = make_uint2(l[0], l[1]);
+}
+
+template <int M, int PB>
+__device__ inline void read_pair_bf(const uint16_t *reg, int kp, int j, int g, int c, bf8 &bh,
+                                    bf8 &bl)
+{
+    const uint16_t *p = reg + (16 * j + c) * PB + 32 * kp + 4 * g;
+    const uint2 a0 = *reinterpret_cast<const uint2 *>(p);
+    const uint2 a1 = *reinterpret_cast<const uint2 *>(p + 16);
+    const uint2 b0 = *reinterpret_cast<const uint2 *>(p + M * PB);
+    const uint2 b1 = *reinterpret_cast<const uint2 *>(p + M * PB + 16);
+    U16B h, l;
+    h.w[0] = a0.x; h.w[1] = a0.y; h.w[2] = a1.x; h.w[3] = a1.y;
+    l.w[0] = b0.x; l.w[1] = b0.y; l.w[2] = b1.x; l.w[3] = b1.y;
+    bh = __builtin_bit_cast(bf8, h);
+    bl = __builtin_bit_cast(bf8, l);
+}
+
+// Left operand of a 32-deep product from two transposed row tiles.
+__device__ inline void split_pair(f4 t0, f4 t1, bf8 &hi, bf8 &lo)
+{
+    float x[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        x[i] = t0[i];
+        x[4 + i] = t1[i];
+    }
+    split_bf16(x, hi, lo);
 }
 
 template <class E, int MT, int D, bool BFM>
@@ -322,19 +374,110 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             ninf = fmaxf(ninf, rowmax[w]);
         alpha = 1.0f / (n1 * ninf);
     }
+    f4 eye;   // identity of the m x m block on this wave's diagonal tile
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        eye[i] = (4 * g + i == c && lval) ? 1.f : 0.f;
+    const f4 zero4 = {0.f, 0.f, 0.f, 0.f};
+    f4 ZLT[MT];   // ZLT[j] lane (g,c): Z[16lt + c][16j + 4g + i]
+
+    // bf16 inputs with an even number of landmark tiles run the iteration on the
+    // bf16 matrix cores, every operand carried as hi + lo terms (three products).
+    constexpr bool BFP = BFM && (MT % 2 == 0);
+    if constexpr (BFP) {
+        constexpr int MP = MT / 2, PB = L::PB;
+        uint16_t *Zh = reinterpret_cast<uint16_t *>(Zb), *Yah = reinterpret_cast<uint16_t *>(Ya);
+        uint16_t *Ybh = reinterpret_cast<uint16_t *>(Yb);
+        float *scr = Yb;   // fp32 own-row transposes (rows 16lt .. 16lt+15)
+        // Z_0 = alpha A^T: bf16 copies for the products, an fp32 copy in scr for
+        // this wave's own row.
+#pragma unroll
+        for (int j = 0; j < MT; ++j) {
+            publish_bf<M, PB>(Zh, j, lt, ALT[j] * alpha, g, c);
+            write_tile<P>(scr, j, lt, ALT[j] * alpha, g, c);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < MT; ++j)
+            ZLT[j] = read_lt<P>(scr, lt, j, g, c);
+        bf8 ah[MP], al[MP];
+#pragma unroll
+        for (int kp = 0; kp < MP; ++kp)
+            split_pair(ALT[2 * kp], ALT[2 * kp + 1], ah[kp], al[kp]);
+        auto product = [&](const bf8 *lh, const bf8 *ll, const uint16_t *reg, int j) {
+            f4 acc = zero4;
+#pragma unroll
+            for (int kp = 0; kp < MP; ++kp) {
+                bf8 bh, bl;
+                read_pair_bf<M, PB>(reg, kp, j, g, c, bh, bl);
+                acc = mfma_bf16(lh[kp], bh, acc);
+                acc = mfma_bf16(lh[kp], bl, acc);
+                acc = mfma_bf16(ll[kp], bh, acc);
+            }
+            return acc;
+        };
+        __syncthreads();   // every wave has read its Z_0 row before scr is reused
+        for (int it = 0; it < a.iters; ++it) {
+            f4 X[MT];
+#pragma unroll
+            for (int j = 0; j < MT; ++j)
+                X[j] = product(ah, al, Zh, j);
+#pragma unroll
+            for (int j = 0; j < MT; ++j)
+                write_tile<P>(scr, lt, j, X[j], g, c);
+            wave_sync();
+            bf8 xh[MP], xl[MP];
+#pragma unroll
+            for (int kp = 0; kp < MP; ++kp)
+                split_pair(read_lt<P>(scr, lt, 2 * kp, g, c), read_lt<P>(scr, lt, 2 * kp + 1, g, c),
+                           xh[kp], xl[kp]);
+#pragma unroll
+            for (int j = 0; j < MT; ++j)
+                publish_bf<M, PB>(Yah, lt, j, (j == lt ? eye * 7.f : zero4) - X[j], g, c);
+            __syncthreads();
+            f4 Y[MT];
+#pragma unroll
+            for (int j = 0; j < MT; ++j)
+                Y[j] = (j == lt ? eye * 15.f : zero4) - product(xh, xl, Yah, j);
+#pragma unroll
+            for (int j = 0; j < MT; ++j)
+                publish_bf<M, PB>(Ybh, lt, j, Y[j], g, c);
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < MT; ++j)
+                Y[j] = (j == lt ? eye * 13.f : zero4) - product(xh, xl, Ybh, j);
+#pragma unroll
+            for (int j = 0; j < MT; ++j)
+                publish_bf<M, PB>(Yah, lt, j, Y[j], g, c);
+            __syncthreads();
+            bf8 zh[MP], zl[MP];
+#pragma unroll
+            for (int kp = 0; kp < MP; ++kp)
+                split_pair(ZLT[2 * kp], ZLT[2 * kp + 1], zh[kp], zl[kp]);
+            f4 Zn[MT];
+#pragma unroll
+            for (int j = 0; j < MT; ++j)
+                Zn[j] = product(zh, zl, Yah, j) * 0.25f;
+#pragma unroll
+            for (int j = 0; j < MT; ++j) {
+                publish_bf<M, PB>(Zh, lt, j, Zn[j], g, c);
+                write_tile<P>(scr, lt, j, Zn[j], g, c);
+            }
+            wave_sync();
+#pragma unroll
+            for (int j = 0; j < MT; ++j)
+                ZLT[j] = read_lt<P>(scr, lt, j, g, c);
+            __syncthreads();
+        }
+    } else {
     // Z_0[j][lt] = alpha (A[lt][j])^T, whose D-layout is alpha * ALT[j].
 #pragma unroll
     for (int j = 0; j < MT; ++j)
         write_tile<P>(Zb, j, lt, ALT[j] * alpha, g, c);
     __syncthreads();
-    f4 ZLT[MT];   // ZLT[j] lane (g,c): Z[16lt + c][16j + 4g + i]
 #pragma unroll
     for (int j = 0; j < MT; ++j)
         ZLT[j] = read_lt<P>(Zb, lt, j, g, c);
-    f4 eye;   // identity of the m x m block on this wave's diagonal tile
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-        eye[i] = (4 * g + i == c && lval) ? 1.f : 0.f;
 
     // Iteration: X = A Z; Z <- Z (13I - X (15I - X (7I - X))) / 4, each wave
     // producing its row tile of every product.
@@ -342,15 +485,10 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         f4 X[MT];
 #pragma unroll
         for (int j = 0; j < MT; ++j) {
-            f4 acc = {0.f, 0.f, 0.f, 0.f};
+            f4 acc = zero4;
 #pragma unroll
-            for (int kk = 0; kk < MT; ++kk) {
-                const f4 zr = read_r<P>(Zb, kk, j, g, c);
-                acc = mfma4(ALT[kk][0], zr[0], acc);
-                acc = mfma4(ALT[kk][1], zr[1], acc);
-                acc = mfma4(ALT[kk][2], zr[2], acc);
-                acc = mfma4(ALT[kk][3], zr[3], acc);
-            }
+            for (int kk = 0; kk < MT; ++kk)
+                acc = mm16_acc(ALT[kk], read_r<P>(Zb, kk, j, g, c), acc);
             X[j] = acc;
         }
         // own-row transpose of X through Yb (free at this point)
@@ -364,16 +502,16 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             XLT[j] = read_lt<P>(Yb, lt, j, g, c);
 #pragma unroll
         for (int j = 0; j < MT; ++j)
-            write_tile<P>(Ya, lt, j, (j == lt ? eye * 7.f : f4{0.f, 0.f, 0.f, 0.f}) - X[j], g, c);
+            write_tile<P>(Ya, lt, j, (j == lt ? eye * 7.f : zero4) - X[j], g, c);
         __syncthreads();
         f4 Y[MT];
 #pragma unroll
         for (int j = 0; j < MT; ++j) {
-            f4 acc = {0.f, 0.f, 0.f, 0.f};
+            f4 acc = zero4;
 #pragma unroll
             for (int kk = 0; kk < MT; ++kk)
                 acc = mm16_acc(XLT[kk], read_r<P>(Ya, kk, j, g, c), acc);
-            Y[j] = (j == lt ? eye * 15.f : f4{0.f, 0.f, 0.f, 0.f}) - acc;
+            Y[j] = (j == lt ? eye * 15.f : zero4) - acc;
         }
 #pragma unroll
         for (int j = 0; j < MT; ++j)
@@ -381,11 +519,11 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         __syncthreads();
 #pragma unroll
         for (int j = 0; j < MT; ++j) {
-            f4 acc = {0.f, 0.f, 0.f, 0.f};
+            f4 acc = zero4;
 #pragma unroll
             for (int kk = 0; kk < MT; ++kk)
                 acc = mm16_acc(XLT[kk], read_r<P>(Yb, kk, j, g, c), acc);
-            Y[j] = (j == lt ? eye * 13.f : f4{0.f, 0.f, 0.f, 0.f}) - acc;
+            Y[j] = (j == lt ? eye * 13.f : zero4) - acc;
         }
 #pragma unroll
         for (int j = 0; j < MT; ++j)
@@ -394,7 +532,7 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         f4 Zn[MT];
 #pragma unroll
         for (int j = 0; j < MT; ++j) {
-            f4 acc = {0.f, 0.f, 0.f, 0.f};
+            f4 acc = zero4;
 #pragma unroll
             for (int kk = 0; kk < MT; ++kk)
                 acc = mm16_acc(ZLT[kk], read_r<P>(Ya, kk, j, g, c), acc);
@@ -408,6 +546,7 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         for (int j = 0; j < MT; ++j)
             ZLT[j] = read_lt<P>(Zb, lt, j, g, c);
         __syncthreads();
+    }
     }
 
     // ---- Steps 5-6 re-associated: W = Z T and W_D = Z T_D.
