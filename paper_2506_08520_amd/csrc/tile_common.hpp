@@ -109,9 +109,21 @@ __device__ inline f4 by_rows(float x, float *vec, int g, int c)
 
 __device__ inline float dpp_xor1(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0xB1, 0xF, 0xF, false); }
 __device__ inline float dpp_xor2(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0x4E, 0xF, 0xF, false); }
-__device__ inline float dpp_ror4(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0x124, 0xF, 0xF, false); }
+// Row rotations read a valid lane everywhere, so bound_ctrl is immaterial;
+// setting it lets the compiler fold the move into the consuming instruction.
+__device__ inline float dpp_ror4(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0x124, 0xF, 0xF, true); }
 // Rotating a 16-lane row by 8 is the exchange of lanes c and c ^ 8.
-__device__ inline float dpp_xor8(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0x128, 0xF, 0xF, false); }
+__device__ inline float dpp_xor8(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0x128, 0xF, 0xF, true); }
+
+// Value of lane (lane & 16) | src within each 32-lane half: with src < 16,
+// every lane of a 16-lane row receives the value of that row's lane src.
+template <int SRC>
+__device__ inline float row_bcast(float x)
+{
+    static_assert(SRC >= 0 && SRC < 16, "source lane within the row");
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x),
+                                                                 0x10 | (SRC << 5)));
+}
 __device__ inline float swz_xor4(float x)
 {
     return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x101F));
@@ -211,6 +223,36 @@ __device__ inline bf8 load_chunk8_bf8(const uint16_t *row, int g)
         if (!slot_valid<D>(g, 2 * j))
             u.w[j] = 0u;
     return __builtin_bit_cast(bf8, u);
+}
+
+// Slot s of lane group g carries a feature that no lower group carries; the
+// chunk of the last, partial group (f0 = D - 8) overlaps the one below it.
+// Equivalent to slot_valid, written so that D-dependent parts fold.
+template <int D>
+__device__ inline bool slot_keep(int g, int s)
+{
+    if constexpr (D % 8 == 0)
+        return g < D / 8;
+    else
+        return s >= 8 - D % 8 ? g <= D / 8 : g < D / 8;
+}
+
+// The eight row elements of a chunk, unmasked (overlapping slots included).
+template <int D>
+__device__ inline void load_row8(const float *p, float *out)
+{
+    const U16B a = *reinterpret_cast<const U16B *>(p);
+    const U16B b = *reinterpret_cast<const U16B *>(p + 4);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        out[j] = __uint_as_float(a.w[j]);
+        out[4 + j] = __uint_as_float(b.w[j]);
+    }
+}
+
+__device__ inline bf8 load_row8_bf16(const uint16_t *p)
+{
+    return __builtin_bit_cast(bf8, *reinterpret_cast<const U16B *>(p));
 }
 
 __device__ inline void unpack_bf8(bf8 v, float *out)

@@ -1,14 +1,20 @@
 // MFMA-tiled PnP-Nystra kernel for small windows (N = 16, 32 or 64 tokens,
 // m <= 16 landmarks, d_h in {8, 16, 24, 30, 32}): one wavefront computes one
-// (window, head) unit entirely in registers, with every contraction on the
-// fp32 matrix cores (v_mfma_f32_16x16x4f32, register tiles in the D-layout
-// of tile_common.hpp) and LDS used only for a few small exchanges.
+// (window, head) unit entirely in registers (register tiles in the D-layout of
+// tile_common.hpp), with LDS used only for a few small exchanges.  fp32 inputs
+// run every contraction on v_mfma_f32_16x16x4f32; bf16 inputs run the
+// products with Q, K and V on v_mfma_f32_16x16x32_bf16, the fp32 partner
+// operand split into bf16 hi + lo terms, and keep S_A, the pseudo-inverse
+// and W = Z T in fp32.
 //
 // Contractions over the feature dimension (S_L, S_U, S_A) use eight MFMA
 // steps in which each lane group supplies a chunk of 8 consecutive features
-// of one token row, loaded straight from global memory in 16-byte pieces
-// (see load_chunk8).  All global loads are branch-free and in bounds, so the
-// compiler can keep every load of a unit in flight at once.
+// of one token row, loaded straight from global memory in 16-byte pieces.
+// The last group's chunk is shifted back to end at the row end, so it
+// overlaps the group below; the overlap is zeroed on the landmark side, and
+// all global loads are branch-free and in bounds.  When d_h leaves a spare
+// column in the last 16-wide feature tile, that column of V is replaced by
+// ones, so the value products also carry the denominators T_D, W_D and O_D.
 #include "internal.hpp"
 #include "tile_common.hpp"
 
@@ -20,31 +26,40 @@ using namespace tile;
 constexpr int kWavesPerBlock = 4;
 constexpr int kLdsPerWave = 2 * 16 * kLdStride + 16 * kTrStride + 64;
 
-// Step 1 for one input: writes the patch means of this wave's tokens to
-// bar[l][f] (LDS).  A patch is the set of tokens that agree with its base
-// token outside the bit mask `free_bits` (the geometry is restricted to powers
-// of two): tile bits are summed within the lane, lane bits across lanes by
-// DPP / swizzle exchanges, one base tile (8 registers) at a time.
-template <int NT, int D>
-__device__ inline void pool_to_lds(const float (&x)[NT][8], float *bar, int free_bits,
-                                   int lg_cols, int lg_pr, int lg_pc, int lg_gc, float inv,
-                                   int g, int c)
+struct SmallArgs {
+    int64_t units;
+    int m, iters;
+    float s2;          // logit scale in base-2 units (scale * log2 e)
+    float inv_patch;   // 1 / tokens per pooling patch (a power of two)
+    int lg_cols, lg_pr, lg_pc, lg_gc, free_bits;   // pooling grid (log2 sizes)
+};
+
+// Step 1 for one input: the patch sums of this wave's tokens (the mean times
+// the patch size; the factor is folded into the logit scales, exactly, since
+// the patch size is a power of two), written to bar[l][8g + s] in the slot
+// layout of the feature chunks with the overlapping slots zeroed.  A patch is
+// the set of tokens that agree with its base token outside the bit mask
+// `free_bits`: tile bits are summed within the lane, lane bits across lanes by
+// DPP / swizzle exchanges.  get(tt, x) yields the eight chunk values of tile tt.
+template <int NT, int D, class Get>
+__device__ inline void pool_to_lds(Get get, float *bar, const SmallArgs &a, int g, int c)
 {
-    const int lane_bits = free_bits & 15, tile_bits = free_bits >> 4;
+    const int lane_bits = a.free_bits & 15, tile_bits = a.free_bits >> 4;
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt) {
         if (tt & tile_bits)
             continue;   // uniform: only base tiles of a patch produce a sum
         float acc[8];
-#pragma unroll
-        for (int s = 0; s < 8; ++s)
-            acc[s] = x[tt][s];
+        get(tt, acc);
 #pragma unroll
         for (int u = 0; u < NT; ++u)
-            if (u != tt && ((u ^ tt) & ~tile_bits) == 0)
+            if (u != tt && ((u ^ tt) & ~tile_bits) == 0) {
+                float y[8];
+                get(u, y);
 #pragma unroll
                 for (int s = 0; s < 8; ++s)
-                    acc[s] += x[u][s];
+                    acc[s] += y[s];
+            }
         if (lane_bits & 1)
 #pragma unroll
             for (int s = 0; s < 8; ++s)
@@ -61,25 +76,26 @@ __device__ inline void pool_to_lds(const float (&x)[NT][8], float *bar, int free
 #pragma unroll
             for (int s = 0; s < 8; ++s)
                 acc[s] += dpp_xor8(acc[s]);
-        const int t = 16 * tt + c;
-        if ((t & free_bits) == 0) {
-            const int r = t >> lg_cols, cc = t & ((1 << lg_cols) - 1);
-            const int l = ((r >> lg_pr) << lg_gc) + (cc >> lg_pc);
 #pragma unroll
-            for (int s = 0; s < 8; ++s)
-                if (slot_valid<D>(g, s))
-                    bar[l * kLdStride + chunk_start<D>(g) + s] = acc[s] * inv;
+        for (int s = 0; s < 8; ++s)
+            acc[s] = slot_keep<D>(g, s) ? acc[s] : 0.f;
+        const int t = 16 * tt + c;
+        if ((t & a.free_bits) == 0) {
+            const int r = t >> a.lg_cols, cc = t & ((1 << a.lg_cols) - 1);
+            const int l = ((r >> a.lg_pr) << a.lg_gc) + (cc >> a.lg_pc);
+            f4 *dst = reinterpret_cast<f4 *>(bar + l * kLdStride + 8 * g);
+            dst[0] = f4{acc[0], acc[1], acc[2], acc[3]};
+            dst[1] = f4{acc[4], acc[5], acc[6], acc[7]};
         }
     }
 }
 
-struct SmallArgs {
-    int64_t units;
-    int m, iters;
-    float s2;          // logit scale in base-2 units (scale * log2 e)
-    float inv_patch;   // 1 / tokens per pooling patch
-    int lg_cols, lg_pr, lg_pc, lg_gc, free_bits;   // pooling grid (log2 sizes)
-};
+__device__ inline uint32_t pack_bf16x2(float lo, float hi)
+{
+    typedef float f2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2{lo, hi}), b2));   // RNE
+}
 
 template <class E, int NT, int D, bool BFM>
 __global__ void __launch_bounds__(64 * kWavesPerBlock)
@@ -87,118 +103,107 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                    const typename E::T *__restrict__ v, typename E::T *__restrict__ o,
                    SmallArgs a)
 {
-    __shared__ float lds_all[kWavesPerBlock * kLdsPerWave];
+    constexpr int N = 16 * NT;
+    constexpr int NCT = (D + 15) / 16;   // 16-wide feature tiles of V, T, W and O
+    // With a spare feature column (D not a multiple of 16), column D of V is
+    // replaced by ones, so that column D of T, W and O carries T_D, W_D, O_D.
+    constexpr bool PAD = D % 16 != 0;
+    __shared__ __attribute__((aligned(16))) float lds_all[kWavesPerBlock * kLdsPerWave];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int g = lane >> 4, c = lane & 15;
     const int64_t unit = int64_t(blockIdx.x) * kWavesPerBlock + wave;
     if (unit >= a.units)
         return;   // whole wavefront; the kernel has no block-level barrier
-    constexpr int N = 16 * NT;
-    constexpr int d = D;
     const int m = a.m;
     float *qbar = lds_all + wave * kLdsPerWave;
     float *kbar = qbar + 16 * kLdStride;
     float *scr = kbar + 16 * kLdStride;
     float *vec = scr + 16 * kTrStride;
 
-    const int64_t base = unit * int64_t(N) * d;
+    const int64_t base = unit * int64_t(N) * D;
     const typename E::T *qu = q + base, *ku = k + base, *vu = v + base;
     typename E::T *ou = o + base;
 
-    // ---- Step 1: load token rows (features 8g..8g+7 of token 16tt+c) and pool.
-    // bf16 inputs (BFM) keep their raw bits for the bf16 matrix cores.
+    // ---- Step 1 loads: chunk (features f0(g).., token 16tt+c) of Q and K;
+    // bf16 inputs keep their raw bits for the bf16 matrix cores.
+    const int f0 = chunk_start<D>(g);
     float qr[NT][8], kr[NT][8];
     bf8 qw[NT], kw[NT];
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt) {
-        const int64_t row = int64_t(16 * tt + c) * d;
+        const int off = (16 * tt + c) * D + f0;
         if constexpr (BFM) {
-            qw[tt] = load_chunk8_bf8<D>(reinterpret_cast<const uint16_t *>(qu) + row, g);
-            kw[tt] = load_chunk8_bf8<D>(reinterpret_cast<const uint16_t *>(ku) + row, g);
+            qw[tt] = load_row8_bf16(reinterpret_cast<const uint16_t *>(qu) + off);
+            kw[tt] = load_row8_bf16(reinterpret_cast<const uint16_t *>(ku) + off);
         } else {
-            load_chunk8<E, D>(qu + row, g, qr[tt]);
-            load_chunk8<E, D>(ku + row, g, kr[tt]);
+            load_row8<D>(qu + off, qr[tt]);
+            load_row8<D>(ku + off, kr[tt]);
         }
     }
     // V in the right-hand operand layout of T = G_U^n V: vr[tt][ct][s] =
-    // V[token 16tt+4g+s][feature 16ct+c] (zero past d).  Issued together with
-    // Q and K so that all of the unit's loads are in flight at once.
-    float vr[NT][2][4];
-    uint16_t vh[NT][2][4];
+    // V[token 16tt+4g+s][feature 16ct+c].  Columns past D read column D-1 and
+    // never reach a stored output; column D becomes the ones column.
+    float vr[NT][NCT][4];
+    uint16_t vh[NT][NCT][4];
 #pragma unroll
-    for (int tt = 0; tt < NT; ++tt)
+    for (int ct = 0; ct < NCT; ++ct) {
+        const int f = 16 * ct + c;
+        const int vlane = 4 * g * D + min(f, D - 1);
 #pragma unroll
-        for (int ct = 0; ct < 2; ++ct) {
-            const int f = 16 * ct + c;
+        for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
-                const int64_t idx = int64_t(16 * tt + 4 * g + s) * d + min(f, d - 1);
+                const int idx = vlane + (16 * tt + s) * D;
+                const bool ones = PAD && ct == NCT - 1 && f == D;
                 if constexpr (BFM) {
                     const uint16_t x = reinterpret_cast<const uint16_t *>(vu)[idx];
-                    vh[tt][ct][s] = f < d ? x : uint16_t(0);
+                    vh[tt][ct][s] = ones ? uint16_t(0x3F80) : x;   // bf16 1.0
                 } else {
                     const float x = E::load(vu, idx);
-                    vr[tt][ct][s] = f < d ? x : 0.f;
+                    vr[tt][ct][s] = ones ? 1.f : x;
                 }
             }
-        }
-    __builtin_amdgcn_sched_barrier(0);
-    if constexpr (BFM) {
-#pragma unroll
-        for (int tt = 0; tt < NT; ++tt) {
-            unpack_bf8(qw[tt], qr[tt]);
-            unpack_bf8(kw[tt], kr[tt]);
-        }
     }
+    __builtin_amdgcn_sched_barrier(0);
+
     // Landmark rows m..15 are padding: zero them so they contribute nothing.
     for (int idx = lane; idx < (16 - m) * 32; idx += 64) {
         const int r = m + idx / 32, f = idx % 32;
         qbar[r * kLdStride + f] = 0.f;
         kbar[r * kLdStride + f] = 0.f;
     }
-    pool_to_lds<NT, D>(qr, qbar, a.free_bits, a.lg_cols, a.lg_pr, a.lg_pc, a.lg_gc,
-                       a.inv_patch, g, c);
-    pool_to_lds<NT, D>(kr, kbar, a.free_bits, a.lg_cols, a.lg_pr, a.lg_pc, a.lg_gc,
-                       a.inv_patch, g, c);
+    if constexpr (BFM) {
+        pool_to_lds<NT, D>([&](int tt, float *x) { unpack_bf8(qw[tt], x); }, qbar, a, g, c);
+        pool_to_lds<NT, D>([&](int tt, float *x) { unpack_bf8(kw[tt], x); }, kbar, a, g, c);
+    } else {
+        pool_to_lds<NT, D>([&](int tt, float *x) { for (int s = 0; s < 8; ++s) x[s] = qr[tt][s]; },
+                           qbar, a, g, c);
+        pool_to_lds<NT, D>([&](int tt, float *x) { for (int s = 0; s < 8; ++s) x[s] = kr[tt][s]; },
+                           kbar, a, g, c);
+    }
     wave_sync();
-    float kb_a[8], qb_b[8];   // Kbar[c][f0 + s], Qbar[c][f0 + s] (slot layout)
+    // Landmark rows in slot layout: kb[s] = Kbar[c][slot s of group g] (zero
+    // in overlapping slots), qb likewise.
+    float kb[8], qb[8];
+    {
+        const f4 *kp = reinterpret_cast<const f4 *>(kbar + c * kLdStride + 8 * g);
+        const f4 *qp = reinterpret_cast<const f4 *>(qbar + c * kLdStride + 8 * g);
+        const f4 k0 = kp[0], k1 = kp[1], q0 = qp[0], q1 = qp[1];
 #pragma unroll
-    for (int s = 0; s < 8; ++s) {
-        const bool ok = slot_valid<D>(g, s);
-        const int f = chunk_start<D>(g) + s;
-        kb_a[s] = ok ? kbar[c * kLdStride + f] : 0.f;
-        qb_b[s] = ok ? qbar[c * kLdStride + f] : 0.f;
+        for (int s = 0; s < 4; ++s) {
+            kb[s] = k0[s];
+            kb[4 + s] = k1[s];
+            qb[s] = q0[s];
+            qb[4 + s] = q1[s];
+        }
     }
     bf8 kbh, kbl, qbh, qbl;   // bf16 path: landmark rows as hi + lo terms
     if constexpr (BFM) {
-        split_bf16(kb_a, kbh, kbl);
-        split_bf16(qb_b, qbh, qbl);
+        split_bf16(kb, kbh, kbl);
+        split_bf16(qb, qbh, qbl);
     }
-
-    // ---- Step 3, G_L side: S_L^T tiles, row max over landmarks, G_L^n.
-    // glT[tt] lane (g,c): G_L^n[token 16tt+c][landmark 4g+i].
-    f4 glT[NT];
-#pragma unroll
-    for (int tt = 0; tt < NT; ++tt) {
-        f4 acc = {0.f, 0.f, 0.f, 0.f};
-        if constexpr (BFM) {
-            acc = mfma_bf16(kbh, qw[tt], acc);
-            acc = mfma_bf16(kbl, qw[tt], acc);
-        } else {
-#pragma unroll
-            for (int s = 0; s < 8; ++s)
-                acc = mfma4(kb_a[s], qr[tt][s], acc);
-        }
-        float mx = -INFINITY;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            if (4 * g + i < m)
-                mx = fmaxf(mx, acc[i]);
-        mx = a.s2 * max_groups(mx);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            glT[tt][i] = (4 * g + i < m) ? fast_exp2(fmaf(a.s2, acc[i], -mx)) : 0.f;
-    }
+    const float s2u = a.s2 * a.inv_patch;    // one pooled side (S_L, S_U)
+    const float s2a = s2u * a.inv_patch;     // both sides pooled (S_A)
 
     // ---- Step 3, G_U side: S_U^T tiles, row max over all N tokens, G_U^n.
     // guT[tt] lane (g,c): G_U^n[landmark c][token 16tt+4g+i].
@@ -213,31 +218,32 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         } else {
 #pragma unroll
             for (int s = 0; s < 8; ++s)
-                acc = mfma4(kr[tt][s], qb_b[s], acc);
+                acc = mfma4(kr[tt][s], qb[s], acc);
         }
         guT[tt] = acc;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            mu = fmaxf(mu, acc[i]);
+        mu = fmaxf(mu, fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3])));
     }
-    mu = a.s2 * max_groups(mu);     // m_U of landmark c (base-2 units)
-    float tden = 0.f;                 // row sum of G_U^n for landmark c
+    mu = s2u * max_groups(mu);     // m_U of landmark c (base-2 units)
+    float tden = 0.f;               // row sum of G_U^n (without a ones column)
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const float e = (c < m) ? fast_exp2(fmaf(a.s2, guT[tt][i], -mu)) : 0.f;
+            const float e = (c < m) ? fast_exp2(fmaf(s2u, guT[tt][i], -mu)) : 0.f;
             guT[tt][i] = e;
             tden += e;
         }
-    tden = sum_groups(tden);
+    if constexpr (!PAD)
+        tden = sum_groups(tden);
 
-    // ---- Step 6, first product: T = G_U^n V  (16 landmarks x 32 features).
-    // T[ct] lane (g,c): T[landmark 4g+i][feature 16ct+c].
-    f4 T[2];
+    // ---- Step 6, first product: T = G_U^n [V | 1]  (16 landmarks x 16 NCT).
+    // T[ct] lane (g,c): T[landmark 4g+i][column 16ct+c].
+    f4 T[NCT];
     if constexpr (BFM) {
         // token tiles in pairs: lane group g supplies tokens 4g..4g+3 of both
-        T[0] = T[1] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct)
+            T[ct] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int tp = 0; tp < (NT + 1) / 2; ++tp) {
             const int t1 = 2 * tp + 1;
@@ -250,7 +256,7 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             bf8 gh, gl;
             split_bf16(g8, gh, gl);
 #pragma unroll
-            for (int ct = 0; ct < 2; ++ct) {
+            for (int ct = 0; ct < NCT; ++ct) {
                 uint16_t v8[8];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
@@ -264,7 +270,7 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         }
     } else {
 #pragma unroll
-        for (int ct = 0; ct < 2; ++ct) {
+        for (int ct = 0; ct < NCT; ++ct) {
             f4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int tt = 0; tt < NT; ++tt)
@@ -275,16 +281,41 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         }
     }
 
+    // ---- Step 3, G_L side: S_L^T tiles, row max over landmarks, G_L^n.
+    // glT[tt] lane (g,c): G_L^n[token 16tt+c][landmark 4g+i].
+    f4 glT[NT];
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt) {
+        f4 acc = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (BFM) {
+            acc = mfma_bf16(kbh, qw[tt], acc);
+            acc = mfma_bf16(kbl, qw[tt], acc);
+        } else {
+#pragma unroll
+            for (int s = 0; s < 8; ++s)
+                acc = mfma4(kb[s], qr[tt][s], acc);
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (4 * g + i < m)
+                mx = fmaxf(mx, acc[i]);
+        mx = s2u * max_groups(mx);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            glT[tt][i] = (4 * g + i < m) ? fast_exp2(fmaf(s2u, acc[i], -mx)) : 0.f;
+    }
+
     // ---- Step 2: G_A^n (rows scaled by m_U).  AT lane (g,c): A[c][4g+i].
     f4 AT;
     {
         f4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int s = 0; s < 8; ++s)
-            acc = mfma4(kb_a[s], qb_b[s], acc);
+            acc = mfma4(kb[s], qb[s], acc);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-            AT[i] = (c < m && 4 * g + i < m) ? fast_exp2(fmaf(a.s2, acc[i], -mu)) : 0.f;
+            AT[i] = (c < m && 4 * g + i < m) ? fast_exp2(fmaf(s2a, acc[i], -mu)) : 0.f;
     }
 
     // ---- Step 4: Z_0 = A^T / (||A||_1 ||A||_inf), then the iteration
@@ -311,57 +342,89 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         ZT = transpose16(Z, scr, g, c);
     }
 
-    // ---- Steps 5-6 re-associated: W = Z T (and its denominator column).
-    f4 Wt[2];
+    // ---- Steps 5-6 re-associated: W = Z T (with the denominator column).
+    f4 Wt[NCT];
 #pragma unroll
-    for (int ct = 0; ct < 2; ++ct)
+    for (int ct = 0; ct < NCT; ++ct)
         Wt[ct] = mm16(ZT, T[ct]);
-    float wden;
-    {
+    f4 wd = {0.f, 0.f, 0.f, 0.f};   // W_D[4g+i] (without a ones column)
+    if constexpr (!PAD) {
         const f4 td = by_rows(tden, vec, g, c);                    // T_D[4g+i]
-        wden = sum_groups(ZT[0] * td[0] + ZT[1] * td[1] + ZT[2] * td[2] + ZT[3] * td[3]);
+        const float wden =
+            sum_groups(ZT[0] * td[0] + ZT[1] * td[1] + ZT[2] * td[2] + ZT[3] * td[3]);
+        wd = by_rows(wden, vec, g, c);
     }
-    const f4 wd = by_rows(wden, vec, g, c);                        // W_D[4g+i]
     // bf16 path: W as hi + lo terms (landmark slots 4g..4g+3, upper half zero).
-    bf8 wh[2], wl[2];
+    bf8 wh[NCT], wl[NCT];
     if constexpr (BFM) {
 #pragma unroll
-        for (int ct = 0; ct < 2; ++ct) {
+        for (int ct = 0; ct < NCT; ++ct) {
             const float w8[8] = {Wt[ct][0], Wt[ct][1], Wt[ct][2], Wt[ct][3], 0.f, 0.f, 0.f, 0.f};
             split_bf16(w8, wh[ct], wl[ct]);
         }
     }
 
     // ---- Steps 3 (G_L side), 6 and 7 per token tile: O = G_L^n W / O_D.
+    const int olane = 4 * g * D + c;
+    const bool odd = c & 1;
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt) {
-        const float od = sum_groups(glT[tt][0] * wd[0] + glT[tt][1] * wd[1] +
-                                      glT[tt][2] * wd[2] + glT[tt][3] * wd[3]);
-        const f4 odr = by_rows(od, vec, g, c);                     // O_D[16tt+4g+i]
-        f4 rcp;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            rcp[i] = __builtin_amdgcn_rcpf(odr[i]);
+        f4 on[NCT];
         bf8 gh, gl;
         if constexpr (BFM) {
             const float g8[8] = {glT[tt][0], glT[tt][1], glT[tt][2], glT[tt][3], 0.f, 0.f, 0.f, 0.f};
             split_bf16(g8, gh, gl);
         }
 #pragma unroll
-        for (int ct = 0; ct < 2; ++ct) {
-            f4 on;
+        for (int ct = 0; ct < NCT; ++ct) {
             if constexpr (BFM) {
-                on = mfma_bf16(gh, wh[ct], f4{0.f, 0.f, 0.f, 0.f});
-                on = mfma_bf16(gh, wl[ct], on);
-                on = mfma_bf16(gl, wh[ct], on);
+                on[ct] = mfma_bf16(gh, wh[ct], f4{0.f, 0.f, 0.f, 0.f});
+                on[ct] = mfma_bf16(gh, wl[ct], on[ct]);
+                on[ct] = mfma_bf16(gl, wh[ct], on[ct]);
             } else {
-                on = mm16(glT[tt], Wt[ct]);
+                on[ct] = mm16(glT[tt], Wt[ct]);
             }
-            const int f = 16 * ct + c;
-            if (f < d) {
+        }
+        f4 rcp;   // 1 / O_D[16tt+4g+i]
+        if constexpr (PAD) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                rcp[i] = __builtin_amdgcn_rcpf(row_bcast<D % 16>(on[NCT - 1][i]));
+        } else {
+            const float od = sum_groups(glT[tt][0] * wd[0] + glT[tt][1] * wd[1] +
+                                        glT[tt][2] * wd[2] + glT[tt][3] * wd[3]);
+            const f4 odr = by_rows(od, vec, g, c);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                rcp[i] = __builtin_amdgcn_rcpf(odr[i]);
+        }
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct) {
+            f4 x;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                x[i] = on[ct][i] * rcp[i];
+            if constexpr (BFM) {
+                // Lanes c and c^1 trade halves: the even lane stores rows 0 and
+                // 2 of features (c, c+1), the odd lane rows 1 and 3 of (c-1, c).
+                f4 nb;
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    E::store(ou, int64_t(16 * tt + 4 * g + i) * d + f, on[i] * rcp[i]);
+                    nb[i] = dpp_xor1(x[i]);
+                const uint32_t p0 = odd ? pack_bf16x2(nb[1], x[1]) : pack_bf16x2(x[0], nb[0]);
+                const uint32_t p1 = odd ? pack_bf16x2(nb[3], x[3]) : pack_bf16x2(x[2], nb[2]);
+                const int fe = 16 * ct + (c & ~1);
+                if (fe < D) {
+                    uint16_t *dst = reinterpret_cast<uint16_t *>(ou) + (4 * g + int(odd)) * D + fe;
+                    *reinterpret_cast<uint32_t *>(dst + 16 * tt * D) = p0;
+                    *reinterpret_cast<uint32_t *>(dst + (16 * tt + 2) * D) = p1;
+                }
+            } else {
+                if (16 * ct + c < D) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        E::store(ou, olane + (16 * tt + i) * D + 16 * ct, x[i]);
+                }
             }
         }
     }
@@ -418,8 +481,8 @@ bool small_supported(const Problem &p)
         return false;
     if (!is_pow2(g.cols) || !is_pow2(g.pr) || !is_pow2(g.pc) || !is_pow2(g.gc))
         return false;
-    if (p.dtype == 1) {   // 16-byte row pieces of bf16 need 4-byte aligned rows
-        const uintptr_t mis = uintptr_t(p.q) | uintptr_t(p.k) | uintptr_t(p.v);
+    if (p.dtype == 1) {   // 16-byte row pieces and paired bf16 stores need 4-byte alignment
+        const uintptr_t mis = uintptr_t(p.q) | uintptr_t(p.k) | uintptr_t(p.v) | uintptr_t(p.o);
         if (mis % 4 != 0)
             return false;
     }
