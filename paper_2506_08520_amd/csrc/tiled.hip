@@ -24,7 +24,20 @@ namespace {
 using namespace tile;
 
 constexpr int kWavesPerBlock = 4;
-constexpr int kLdsPerWave = 2 * 16 * kLdStride + 16 * kTrStride + 64;
+typedef __attribute__((address_space(1))) void global_void;
+typedef __attribute__((address_space(3))) void lds_void;
+
+// LDS of one wave: the landmark rows of Q and K (slot layout), a stage that
+// holds V (row-major, as in memory), then the transpose scratch of the
+// pseudo-inverse, then O before its contiguous store, and a row vector.
+template <class E, int NT, int D>
+struct SmallLds {
+    static constexpr int kBlockFloats = 16 * NT * D * E::bytes / 4;   // one unit's V or O
+    static constexpr int kStage =
+        ((kBlockFloats > 16 * kTrStride ? kBlockFloats : 16 * kTrStride) + 3) / 4 * 4;
+    static constexpr int kPerWave = 2 * 16 * kLdStride + kStage + 64;
+    static constexpr int kPieces = 16 * NT * D * E::bytes / 16;       // 16-byte pieces of V or O
+};
 
 struct SmallArgs {
     int64_t units;
@@ -108,17 +121,19 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     // With a spare feature column (D not a multiple of 16), column D of V is
     // replaced by ones, so that column D of T, W and O carries T_D, W_D, O_D.
     constexpr bool PAD = D % 16 != 0;
-    __shared__ __attribute__((aligned(16))) float lds_all[kWavesPerBlock * kLdsPerWave];
+    using L = SmallLds<E, NT, D>;
+    __shared__ __attribute__((aligned(16))) float lds_all[kWavesPerBlock * L::kPerWave];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int g = lane >> 4, c = lane & 15;
     const int64_t unit = int64_t(blockIdx.x) * kWavesPerBlock + wave;
     if (unit >= a.units)
         return;   // whole wavefront; the kernel has no block-level barrier
     const int m = a.m;
-    float *qbar = lds_all + wave * kLdsPerWave;
+    float *qbar = lds_all + wave * L::kPerWave;
     float *kbar = qbar + 16 * kLdStride;
-    float *scr = kbar + 16 * kLdStride;
-    float *vec = scr + 16 * kTrStride;
+    float *stage = kbar + 16 * kLdStride;
+    float *scr = stage;   // transpose scratch once V has been read
+    float *vec = stage + L::kStage;
 
     const int64_t base = unit * int64_t(N) * D;
     const typename E::T *qu = q + base, *ku = k + base, *vu = v + base;
@@ -140,29 +155,15 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             load_row8<D>(ku + off, kr[tt]);
         }
     }
-    // V in the right-hand operand layout of T = G_U^n V: vr[tt][ct][s] =
-    // V[token 16tt+4g+s][feature 16ct+c].  Columns past D read column D-1 and
-    // never reach a stored output; column D becomes the ones column.
-    float vr[NT][NCT][4];
-    uint16_t vh[NT][NCT][4];
+    // V: the unit's contiguous block, copied to the stage by 16-byte direct
+    // loads (lane l of a round writes piece l of that round).
+    {
+        const char *vb = reinterpret_cast<const char *>(vu);
 #pragma unroll
-    for (int ct = 0; ct < NCT; ++ct) {
-        const int f = 16 * ct + c;
-        const int vlane = 4 * g * D + min(f, D - 1);
-#pragma unroll
-        for (int tt = 0; tt < NT; ++tt)
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                const int idx = vlane + (16 * tt + s) * D;
-                const bool ones = PAD && ct == NCT - 1 && f == D;
-                if constexpr (BFM) {
-                    const uint16_t x = reinterpret_cast<const uint16_t *>(vu)[idx];
-                    vh[tt][ct][s] = ones ? uint16_t(0x3F80) : x;   // bf16 1.0
-                } else {
-                    const float x = E::load(vu, idx);
-                    vr[tt][ct][s] = ones ? 1.f : x;
-                }
-            }
+        for (int p0 = 0; p0 < L::kPieces; p0 += 64)
+            if (p0 + 64 <= L::kPieces || p0 + lane < L::kPieces)
+                __builtin_amdgcn_global_load_lds((global_void *)(vb + 16 * (p0 + lane)),
+                                                 (lds_void *)(stage + 4 * p0), 16, 0, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
 
@@ -235,6 +236,34 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         }
     if constexpr (!PAD)
         tden = sum_groups(tden);
+
+    // V in the right-hand operand layout of T = G_U^n V: vr[tt][ct][s] =
+    // V[token 16tt+4g+s][feature 16ct+c].  Columns past D read column D-1 and
+    // never reach a stored output; column D becomes the ones column.
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): the stage holds V
+    wave_sync();
+    float vr[NT][NCT][4];
+    uint16_t vh[NT][NCT][4];
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) {
+        const int f = 16 * ct + c;
+        const int vlane = 4 * g * D + min(f, D - 1);
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const int idx = vlane + (16 * tt + s) * D;
+                const bool ones = PAD && ct == NCT - 1 && f == D;
+                if constexpr (BFM) {
+                    const uint16_t x = reinterpret_cast<const uint16_t *>(stage)[idx];
+                    vh[tt][ct][s] = ones ? uint16_t(0x3F80) : x;   // bf16 1.0
+                } else {
+                    const float x = stage[idx];
+                    vr[tt][ct][s] = ones ? 1.f : x;
+                }
+            }
+    }
+    wave_sync();   // the stage is free again (transpose scratch, then O)
 
     // ---- Step 6, first product: T = G_U^n [V | 1]  (16 landmarks x 16 NCT).
     // T[ct] lane (g,c): T[landmark 4g+i][column 16ct+c].
@@ -404,8 +433,9 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 #pragma unroll
             for (int i = 0; i < 4; ++i)
                 x[i] = on[ct][i] * rcp[i];
+            // O goes to the stage row-major (as in memory).
             if constexpr (BFM) {
-                // Lanes c and c^1 trade halves: the even lane stores rows 0 and
+                // Lanes c and c^1 trade halves: the even lane writes rows 0 and
                 // 2 of features (c, c+1), the odd lane rows 1 and 3 of (c-1, c).
                 f4 nb;
 #pragma unroll
@@ -415,7 +445,7 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                 const uint32_t p1 = odd ? pack_bf16x2(nb[3], x[3]) : pack_bf16x2(x[2], nb[2]);
                 const int fe = 16 * ct + (c & ~1);
                 if (fe < D) {
-                    uint16_t *dst = reinterpret_cast<uint16_t *>(ou) + (4 * g + int(odd)) * D + fe;
+                    uint16_t *dst = reinterpret_cast<uint16_t *>(stage) + (4 * g + int(odd)) * D + fe;
                     *reinterpret_cast<uint32_t *>(dst + 16 * tt * D) = p0;
                     *reinterpret_cast<uint32_t *>(dst + (16 * tt + 2) * D) = p1;
                 }
@@ -423,9 +453,21 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                 if (16 * ct + c < D) {
 #pragma unroll
                     for (int i = 0; i < 4; ++i)
-                        E::store(ou, olane + (16 * tt + i) * D + 16 * ct, x[i]);
+                        stage[olane + (16 * tt + i) * D + 16 * ct] = x[i];
                 }
             }
+        }
+    }
+    // ---- Step 7 store: the unit's O block in 16-byte pieces.
+    wave_sync();
+    {
+        char *ob = reinterpret_cast<char *>(ou);
+        const f4 *src = reinterpret_cast<const f4 *>(stage);
+#pragma unroll
+        for (int p0 = 0; p0 < L::kPieces; p0 += 64) {
+            const int p = p0 + lane;
+            if (p0 + 64 <= L::kPieces || p < L::kPieces)
+                *reinterpret_cast<f4 *>(ob + 16 * p) = src[p];
         }
     }
 }
@@ -481,11 +523,12 @@ bool small_supported(const Problem &p)
         return false;
     if (!is_pow2(g.cols) || !is_pow2(g.pr) || !is_pow2(g.pc) || !is_pow2(g.gc))
         return false;
-    if (p.dtype == 1) {   // 16-byte row pieces and paired bf16 stores need 4-byte alignment
-        const uintptr_t mis = uintptr_t(p.q) | uintptr_t(p.k) | uintptr_t(p.v) | uintptr_t(p.o);
-        if (mis % 4 != 0)
-            return false;
-    }
+    // V and O move as whole 16-byte pieces; bf16 row chunks of Q and K are
+    // read as 16-byte pieces that start at even elements.
+    if ((uintptr_t(p.v) | uintptr_t(p.o)) % 16 != 0)
+        return false;
+    if (p.dtype == 1 && (uintptr_t(p.q) | uintptr_t(p.k)) % 4 != 0)
+        return false;
     return true;
 }
 
