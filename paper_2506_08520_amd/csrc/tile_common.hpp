@@ -70,6 +70,49 @@ __device__ inline void split_bf16(const float (&x)[8], bf8 &hi, bf8 &lo)
     }
 }
 
+struct __attribute__((aligned(4))) U16B {
+    uint32_t w[4];
+};
+
+// A D-layout fp32 tile as two bf16 terms, packed as the A operand of a
+// 16x16x32 product over a 16-deep contraction: lane group g supplies, at
+// k = 8g + j, the hi term (j < 4) or the lo term (j >= 4) of its element
+// 4g + (j & 3).  hi = bf16(x) and lo = bf16(x - hi) (round to nearest even).
+struct SplitTile {
+    bf8 hl;   // [hi0..hi3, lo0..lo3]
+};
+
+__device__ inline uint32_t cvt_bf16x2(float lo, float hi)
+{
+    typedef float f2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2{lo, hi}), b2));   // RNE
+}
+
+__device__ inline SplitTile split_tile(f4 x)
+{
+    U16B u;
+    u.w[0] = cvt_bf16x2(x[0], x[1]);
+    u.w[1] = cvt_bf16x2(x[2], x[3]);
+    const float h0 = __uint_as_float(u.w[0] << 16), h1 = __uint_as_float(u.w[0] & 0xffff0000u);
+    const float h2 = __uint_as_float(u.w[1] << 16), h3 = __uint_as_float(u.w[1] & 0xffff0000u);
+    u.w[2] = cvt_bf16x2(x[0] - h0, x[1] - h1);
+    u.w[3] = cvt_bf16x2(x[2] - h2, x[3] - h3);
+    return SplitTile{__builtin_bit_cast(bf8, u)};
+}
+
+// L * R for 16x16 tiles given LT = L^T and R in split form: the two
+// products (L_hi + L_lo) R_hi and (L_hi + L_lo) R_lo on the bf16 matrix
+// cores, accumulated in fp32.
+__device__ inline f4 mm16_split(const SplitTile &LT, const SplitTile &R)
+{
+    const U16B r = __builtin_bit_cast(U16B, R.hl);
+    const U16B rh = {{r.w[0], r.w[1], r.w[0], r.w[1]}};
+    const U16B rl = {{r.w[2], r.w[3], r.w[2], r.w[3]}};
+    const f4 acc = mfma_bf16(LT.hl, __builtin_bit_cast(bf8, rh), f4{0.f, 0.f, 0.f, 0.f});
+    return mfma_bf16(LT.hl, __builtin_bit_cast(bf8, rl), acc);
+}
+
 // Orders the LDS traffic of one wavefront (all lanes execute in lockstep, so
 // only the compiler and the memory counters need fencing).
 __device__ inline void wave_sync()
@@ -172,9 +215,6 @@ __device__ inline float max_row(float x)
     return fmaxf(x, dpp_xor8(x));
 }
 
-struct __attribute__((aligned(4))) U16B {
-    uint32_t w[4];
-};
 
 // Feature chunk of lane group g.  The contraction over features runs as
 // eight MFMA steps in which group g supplies the features in slots s = 0..7.

@@ -4,8 +4,8 @@
 // tile_common.hpp), with LDS used only for a few small exchanges.  fp32 inputs
 // run every contraction on v_mfma_f32_16x16x4f32; bf16 inputs run the
 // products with Q, K and V on v_mfma_f32_16x16x32_bf16, the fp32 partner
-// operand split into bf16 hi + lo terms, and keep S_A, the pseudo-inverse
-// and W = Z T in fp32.
+// operand split into bf16 hi + lo terms, run the pseudo-inverse products as
+// (hi + lo) x (hi + lo) bf16 terms, and keep S_A and W = Z T in fp32.
 //
 // Contractions over the feature dimension (S_L, S_U, S_A) use eight MFMA
 // steps in which each lane group supplies a chunk of 8 consecutive features
@@ -361,14 +361,28 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 #pragma unroll
     for (int i = 0; i < 4; ++i)
         eye[i] = (4 * g + i == c && c < m) ? 1.f : 0.f;
-    for (int it = 0; it < a.iters; ++it) {
-        const f4 X = mm16(AT, Z);
-        const f4 XT = transpose16(X, scr, g, c);
-        f4 Y = eye * 7.f - X;
-        Y = eye * 15.f - mm16(XT, Y);
-        Y = eye * 13.f - mm16(XT, Y);
-        Z = mm16(ZT, Y) * 0.25f;
-        ZT = transpose16(Z, scr, g, c);
+    if constexpr (BFM) {
+        // bf16 inputs: every product as (hi + lo) x (hi + lo) bf16 terms.
+        const SplitTile ATs = split_tile(AT);
+        for (int it = 0; it < a.iters; ++it) {
+            const f4 X = mm16_split(ATs, split_tile(Z));
+            const SplitTile XTs = split_tile(transpose16(X, scr, g, c));
+            f4 Y = eye * 7.f - X;
+            Y = eye * 15.f - mm16_split(XTs, split_tile(Y));
+            Y = eye * 13.f - mm16_split(XTs, split_tile(Y));
+            Z = mm16_split(split_tile(ZT), split_tile(Y)) * 0.25f;
+            ZT = transpose16(Z, scr, g, c);
+        }
+    } else {
+        for (int it = 0; it < a.iters; ++it) {
+            const f4 X = mm16(AT, Z);
+            const f4 XT = transpose16(X, scr, g, c);
+            f4 Y = eye * 7.f - X;
+            Y = eye * 15.f - mm16(XT, Y);
+            Y = eye * 13.f - mm16(XT, Y);
+            Z = mm16(ZT, Y) * 0.25f;
+            ZT = transpose16(Z, scr, g, c);
+        }
     }
 
     // ---- Steps 5-6 re-associated: W = Z T (with the denominator column).
