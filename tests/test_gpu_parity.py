@@ -36,11 +36,11 @@ def run(q, k, v, m, dtype, variant, iters=6, mode=0, scale=0.0):
 def check_config(got, ref, dtype, what):
     """Parity bar for the configuration workloads.
 
-    fp32: max-abs <= 1e-4.  bf16: the error left after allowing each element
-    the half-ulp that rounding the exact result to bf16 costs must be within
-    2e-2 of the output RMS, and within 2e-3 for these workloads (the compute
-    error proper is ~1e-4 of RMS); the literal max-abs / RMS, which bf16
-    storage alone can push to ~2e-2 on heavy-tailed outputs, is printed."""
+    fp32: max-abs <= 1e-4.  bf16: max-abs <= 2e-2 of the output RMS, and in
+    addition the error left after allowing each element the half-ulp that
+    rounding the exact result to bf16 costs must stay within 2e-3 of RMS (the
+    compute error proper is ~1e-4 of RMS; on heavy-tailed outputs the bf16
+    storage alone brings the literal figure close to 2e-2)."""
     if dtype == "f32":
         err = error(got, ref, dtype)
         print(f"{what}: max-abs {err:.3e}")
@@ -49,7 +49,7 @@ def check_config(got, ref, dtype, what):
     lit = error(got, ref, dtype)
     beyond = error(got, ref, dtype, storage_floor=True)
     print(f"{what}: max-abs/RMS {lit:.3e}, beyond bf16 rounding {beyond:.3e}")
-    assert beyond <= TOL[dtype]
+    assert lit <= TOL[dtype]
     assert beyond <= 2e-3
 
 
