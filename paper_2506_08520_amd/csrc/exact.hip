@@ -119,7 +119,7 @@ exact_tiled_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 {
     extern __shared__ uint16_t vt[];   // bf16 only: V^T, [32 features][N + 8 keys]
     constexpr int d = D;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
     const int g = lane >> 4, c = lane & 15;
     const int64_t unit = blockIdx.x / qblocks;
     const int NT = N >> 4, pitch = N + 8;

@@ -123,7 +123,9 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     constexpr bool PAD = D % 16 != 0;
     using L = SmallLds<E, NT, D>;
     __shared__ __attribute__((aligned(16))) float lds_all[kWavesPerBlock * L::kPerWave];
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    // The wave index is uniform across the wavefront; saying so keeps the
+    // unit's base addresses in scalar registers.
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
     const int g = lane >> 4, c = lane & 15;
     const int64_t unit = int64_t(blockIdx.x) * kWavesPerBlock + wave;
     if (unit >= a.units)
