@@ -6,8 +6,9 @@
 //   1. Step 1: each lane averages the patch of its own landmark straight from
 //      global memory (any pooling grid), producing Qbar rows in registers and
 //      Kbar rows in LDS.
-//   2. Step 3, G_U side: the wave streams all N keys twice -- once for the row
-//      maxima m_U of its landmarks, once for G_U^n and T = G_U^n [V | 1].
+//   2. Step 3, G_U side: the wave streams all N keys once, keeping the row
+//      maxima m_U of its landmarks as running maxima and accumulating
+//      G_U^n and T = G_U^n [V | 1], rescaled whenever a maximum grows.
 //   3. Step 2 and Step 4: the wave builds its row tile of A = G_A^n; the m x m
 //      pseudo-inverse iteration runs with each wave computing its row tile of
 //      every product, the right-hand operands exchanged through LDS.
@@ -198,8 +199,11 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         if (slot_valid<D>(g, s))
             kbar[l * kTS + chunk_start<D>(g) + s] = kbv[s];
 
-    // ---- Step 3, G_U side, pass 1: m_U of this landmark over all N keys,
-    // kGroup key tiles per step (a repeated last tile leaves the max unchanged).
+    // ---- Step 3, G_U side, one pass over the N keys, kGroup key tiles per
+    // step: m_U of this landmark as a running maximum, and G_U^n and
+    // T = G_U^n [V | 1] accumulated against it; when the maximum grows, the
+    // partial T and T_D are rescaled by exp(old - new), so that at the end they
+    // hold exactly the sums against the final m_U.
     constexpr int kGroup = 4;
     const uint16_t *ku16 = reinterpret_cast<const uint16_t *>(ku);
     bf8 qbh, qbl;   // bf16 path: Qbar row as hi + lo terms
@@ -218,30 +222,10 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         }
         return acc;
     };
-    float mx = -INFINITY;
-    for (int t0 = 0; t0 < NT; t0 += kGroup) {
-        float kr[kGroup][8];
-        bf8 kw[kGroup];
-#pragma unroll
-        for (int u = 0; u < kGroup; ++u) {
-            const int64_t row = int64_t(16 * min(t0 + u, NT - 1) + c) * d;
-            if constexpr (BFM)
-                kw[u] = load_chunk8_bf8<D>(ku16 + row, g);
-            else
-                load_chunk8<E, D>(ku + row, g, kr[u]);
-        }
-#pragma unroll
-        for (int u = 0; u < kGroup; ++u) {
-            const f4 acc = su_tile(t0 + u, kr[u], kw[u]);
-            mx = fmaxf(mx, fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3])));
-        }
-    }
-    const float mu = a.s2 * max_groups(mx);   // m_U of landmark l (base-2 units)
-
-    // ---- pass 2: G_U^n and T = G_U^n V, T_D = G_U^n 1.
     // T[ct] lane (g,c): T[landmark 16lt+4g+i][feature 16ct+c].
     f4 T[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-    float tden = 0.f;
+    float tden = 0.f;    // this lane's share of T_D of landmark l
+    float mrun = -INFINITY;   // running max of S_U[l][.] (unscaled logits)
     const uint16_t *vu16 = reinterpret_cast<const uint16_t *>(vu);
     for (int t0 = 0; t0 < NT; t0 += kGroup) {
         float kr[kGroup][8], vr[kGroup][2][4];
@@ -271,6 +255,26 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                 }
             }
         }
+        // Logits of the group (a repeated last tile leaves the maximum unchanged
+        // and is not accumulated).
+        f4 su[kGroup];
+        float gmax = -INFINITY;
+#pragma unroll
+        for (int u = 0; u < kGroup; ++u) {
+            su[u] = su_tile(min(t0 + u, NT - 1), kr[u], kw[u]);
+            gmax = fmaxf(gmax, fmaxf(fmaxf(su[u][0], su[u][1]), fmaxf(su[u][2], su[u][3])));
+        }
+        const float mnew = fmaxf(mrun, max_groups(gmax));
+        {   // rescale what is accumulated: factor 1 exactly when the maximum
+            // holds, 0 on the first group (all lanes take part in the exchange)
+            const float f = fast_exp2(a.s2 * (mrun - mnew));
+            tden *= f;
+            const f4 fr = by_rows(f, vec, g, c);   // factor of landmark 16lt+4g+i
+            T[0] *= fr;
+            T[1] *= fr;
+        }
+        mrun = mnew;
+        const float mb = a.s2 * mnew;
         if constexpr (BFM) {
             // Key tiles in pairs: the bf16 product contracts 32 keys, lane group g
             // supplying keys 4g..4g+3 of both tiles.  N % 32 == 0 on this path.
@@ -280,14 +284,12 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                     break;   // uniform
                 float gk[8];
 #pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const f4 acc = su_tile(t0 + u + h, kr[u + h], kw[u + h]);
+                for (int h = 0; h < 2; ++h)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        gk[4 * h + i] = lval ? fast_exp2(fmaf(a.s2, acc[i], -mu)) : 0.f;
+                        gk[4 * h + i] = lval ? fast_exp2(fmaf(a.s2, su[u + h][i], -mb)) : 0.f;
                         tden += gk[4 * h + i];
                     }
-                }
                 bf8 gh, gl;
                 split_bf16(gk, gh, gl);
 #pragma unroll
@@ -307,20 +309,21 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             for (int u = 0; u < kGroup; ++u) {
                 if (t0 + u >= NT)
                     break;   // uniform
-                f4 acc = su_tile(t0 + u, kr[u], kw[u]);
+                f4 e;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    acc[i] = lval ? fast_exp2(fmaf(a.s2, acc[i], -mu)) : 0.f;
-                    tden += acc[i];
+                    e[i] = lval ? fast_exp2(fmaf(a.s2, su[u][i], -mb)) : 0.f;
+                    tden += e[i];
                 }
 #pragma unroll
                 for (int ct = 0; ct < 2; ++ct)
 #pragma unroll
                     for (int s = 0; s < 4; ++s)
-                        T[ct] = mfma4(acc[s], vr[u][ct][s], T[ct]);
+                        T[ct] = mfma4(e[s], vr[u][ct][s], T[ct]);
             }
         }
     }
+    const float mu = a.s2 * mrun;   // m_U of landmark l (base-2 units)
     tden = sum_groups(tden);   // T_D of landmark l
     __syncthreads();           // Kbar complete
 
