@@ -13,25 +13,18 @@ SOURCES = ["abi.hip", "generic.hip", "exact.hip", "tiled.hip", "tiled_large.hip"
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-# Packed-fp32 VALU instructions are kept out of every kernel.
+# Packed-fp32 VALU instructions are kept out of every kernel.  MFMA results
+# are written straight to VGPRs (instead of the accumulation registers), which
+# spares the copies back and lowers the register count of the tiled kernels.
 FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-Wall", "-Werror",
          "-Wno-unused-function", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         "-mllvm", "-amdgpu-mfma-vgpr-form=1",
          "-I", os.path.join(os.path.dirname(HERE), "include")]
-
-
-# Per-file code generation choices.  MFMA results written straight to VGPRs
-# (instead of the accumulation registers) spare the copies back and lower the
-# register count of the small-window and exact kernels; the multi-wave kernel
-# keeps the default, which needs fewer registers there.
-EXTRA = {
-    "tiled.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
-    "exact.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
-}
 
 
 def _compile(src, verbose):
     obj = os.path.join(OBJDIR, src.replace(".hip", ".o"))
-    cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
