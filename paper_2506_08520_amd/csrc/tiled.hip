@@ -52,8 +52,9 @@ struct SmallArgs {
 // the patch size is a power of two), written to bar[l][8g + s] in the slot
 // layout of the feature chunks with the overlapping slots zeroed.  A patch is
 // the set of tokens that agree with its base token outside the bit mask
-// `free_bits`: tile bits are summed within the lane, lane bits across lanes by
-// DPP / swizzle exchanges.  get(tt, x) yields the eight chunk values of tile tt.
+// `free_bits`: tile bits are summed within the lane (base tiles only), lane
+// bits across lanes by DPP / swizzle exchanges.  get(tt, x) yields the eight
+// chunk values of tile tt.
 template <int NT, int D, class Get>
 __device__ inline void pool_to_lds(Get get, float *bar, const SmallArgs &a, int g, int c)
 {
@@ -92,14 +93,15 @@ __device__ inline void pool_to_lds(Get get, float *bar, const SmallArgs &a, int 
 #pragma unroll
         for (int s = 0; s < 8; ++s)
             acc[s] = slot_keep<D>(g, s) ? acc[s] : 0.f;
+        // The exchanges are butterflies of commutative additions, so every
+        // lane of a patch holds the same sum bit for bit: all of them store
+        // it (no branch), each to its own token's landmark row.
         const int t = 16 * tt + c;
-        if ((t & a.free_bits) == 0) {
-            const int r = t >> a.lg_cols, cc = t & ((1 << a.lg_cols) - 1);
-            const int l = ((r >> a.lg_pr) << a.lg_gc) + (cc >> a.lg_pc);
-            f4 *dst = reinterpret_cast<f4 *>(bar + l * kLdStride + 8 * g);
-            dst[0] = f4{acc[0], acc[1], acc[2], acc[3]};
-            dst[1] = f4{acc[4], acc[5], acc[6], acc[7]};
-        }
+        const int r = t >> a.lg_cols, cc = t & ((1 << a.lg_cols) - 1);
+        const int l = ((r >> a.lg_pr) << a.lg_gc) + (cc >> a.lg_pc);
+        f4 *dst = reinterpret_cast<f4 *>(bar + l * kLdStride + 8 * g);
+        dst[0] = f4{acc[0], acc[1], acc[2], acc[3]};
+        dst[1] = f4{acc[4], acc[5], acc[6], acc[7]};
     }
 }
 
@@ -399,14 +401,12 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             sum_groups(ZT[0] * td[0] + ZT[1] * td[1] + ZT[2] * td[2] + ZT[3] * td[3]);
         wd = by_rows(wden, vec, g, c);
     }
-    // bf16 path: W as hi + lo terms (landmark slots 4g..4g+3, upper half zero).
-    bf8 wh[NCT], wl[NCT];
+    // bf16 path: W as hi + lo terms.
+    SplitTile ws[NCT];
     if constexpr (BFM) {
 #pragma unroll
-        for (int ct = 0; ct < NCT; ++ct) {
-            const float w8[8] = {Wt[ct][0], Wt[ct][1], Wt[ct][2], Wt[ct][3], 0.f, 0.f, 0.f, 0.f};
-            split_bf16(w8, wh[ct], wl[ct]);
-        }
+        for (int ct = 0; ct < NCT; ++ct)
+            ws[ct] = split_tile(Wt[ct]);
     }
 
     // ---- Steps 3 (G_L side), 6 and 7 per token tile: O = G_L^n W / O_D.
@@ -415,20 +415,15 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt) {
         f4 on[NCT];
-        bf8 gh, gl;
-        if constexpr (BFM) {
-            const float g8[8] = {glT[tt][0], glT[tt][1], glT[tt][2], glT[tt][3], 0.f, 0.f, 0.f, 0.f};
-            split_bf16(g8, gh, gl);
-        }
+        SplitTile gs;
+        if constexpr (BFM)
+            gs = split_tile(glT[tt]);
 #pragma unroll
         for (int ct = 0; ct < NCT; ++ct) {
-            if constexpr (BFM) {
-                on[ct] = mfma_bf16(gh, wh[ct], f4{0.f, 0.f, 0.f, 0.f});
-                on[ct] = mfma_bf16(gh, wl[ct], on[ct]);
-                on[ct] = mfma_bf16(gl, wh[ct], on[ct]);
-            } else {
+            if constexpr (BFM)
+                on[ct] = mm16_split(gs, ws[ct]);   // (G_hi + G_lo)(W_hi + W_lo)
+            else
                 on[ct] = mm16(glT[tt], Wt[ct]);
-            }
         }
         f4 rcp;   // 1 / O_D[16tt+4g+i]
         if constexpr (PAD) {
