@@ -55,8 +55,10 @@ typedef enum { NYSTRA_F32 = 0, NYSTRA_BF16 = 1 } nystra_dtype;
 typedef enum { NYSTRA_LM_POOL2D = 0, NYSTRA_LM_SEGMENT1D = 1 } nystra_landmark_mode;
 
 /* Kernel family used by nystra_attn_forward_ex.  AUTO picks the MFMA-tiled
- * kernel when the shape is one it covers and the generic kernel otherwise;
- * the other values force one (NYSTRA_ERR_UNSUPPORTED if it cannot run). */
+ * kernel when the shape is one it covers and the pointers are aligned as it
+ * needs (V and O to 16 bytes; for bf16 also Q and K to 4 bytes), and the
+ * generic kernel otherwise; the other values force one
+ * (NYSTRA_ERR_UNSUPPORTED if it cannot run). */
 typedef enum {
     NYSTRA_VARIANT_AUTO = 0,
     NYSTRA_VARIANT_GENERIC = 1,
@@ -127,8 +129,9 @@ int nystra_landmark_pool(const void *Q, const void *K, float *Qbar, float *Kbar,
 int nystra_landmark_map(int N, int m, int mode, int32_t *map_host);
 
 /* Host-only: which kernel family nystra_attn_forward_ex would launch for
- * this shape and options (NYSTRA_VARIANT_GENERIC or NYSTRA_VARIANT_TILED), or a
- * negative nystra_status if the arguments are invalid. */
+ * this shape and options with 16-byte aligned tensors (NYSTRA_VARIANT_GENERIC
+ * or NYSTRA_VARIANT_TILED), or a negative nystra_status if the arguments are
+ * invalid. */
 int nystra_select_variant(int N, int d_h, int m, int dtype, const nystra_opts *opts);
 
 /* Static description of a status code. */

@@ -13,7 +13,7 @@ import pytest
 import oracle
 from paper_2506_08520_amd import binding as B
 from paper_2506_08520_amd import workloads as W
-from helpers import TOL, error, sample_units, to_dev, to_host
+from helpers import torch_dtype, TOL, error, sample_units, to_dev, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -249,6 +249,44 @@ def test_output_untouched_on_validation_error():
         B.nystra_attn_forward_ex(q, k, v, 16, opts=B.make_opts(pinv_iters=99), out=o)
     torch.cuda.synchronize()
     assert bool((o == 7.0).all())
+
+
+# (dtype, element offset, does a tiled kernel take it): fp32 at 4 bytes runs the
+# multi-wave tiled kernel (the 64-token one needs V and O 16-byte aligned), bf16
+# at 2 bytes has no tiled kernel, 16-byte offsets run the 64-token kernel.
+ALIGN = [("f32", 1, True), ("bf16", 1, False), ("f32", 4, True), ("bf16", 8, True)]
+
+
+@pytest.mark.parametrize("dtype,offset,tiled", ALIGN)
+def test_element_aligned_tensors(dtype, offset, tiled):
+    """Tensors offset from their allocation: a forced tiled launch runs when a
+    tiled kernel can take the alignment and is refused before touching O
+    otherwise; AUTO always runs, and results match the oracle."""
+    wl = W.CONFIGS["c2"]
+    q, k, v = W.generate(wl, dtype, n_windows=4)
+    ref = oracle.forward(q, k, v, wl.m, iters=6, mode=0)
+    n = q.size
+    flat = [torch.zeros(n + offset, dtype=torch_dtype(dtype), device="cuda") for _ in range(4)]
+    views = [f[offset:].view(q.shape) for f in flat]
+    for view, x in zip(views[:3], (q, k, v)):
+        view.copy_(to_dev(x, dtype))
+    o = views[3]
+    o.fill_(7.0)
+    forced = B.make_opts(variant=B.VARIANT_TILED)
+    if tiled:
+        B.nystra_attn_forward_ex(*views[:3], wl.m, opts=forced, out=o)
+        torch.cuda.synchronize()
+        check_config(to_host(o), ref, dtype, f"c2 {dtype} offset {offset} tiled")
+        o.fill_(7.0)
+    else:
+        with pytest.raises(B.NystraError) as e:
+            B.nystra_attn_forward_ex(*views[:3], wl.m, opts=forced, out=o)
+        assert e.value.status == 6
+        torch.cuda.synchronize()
+        assert bool((o == 7.0).all())
+    B.nystra_attn_forward_ex(*views[:3], wl.m, opts=B.make_opts(), out=o)
+    torch.cuda.synchronize()
+    check_config(to_host(o), ref, dtype, f"c2 {dtype} offset {offset} auto")
 
 
 def test_empty_batch_is_noop():
