@@ -223,6 +223,26 @@ def test_full_size_exact_sampled(cfg, dtype, count):
     assert error(got[idx], ref, dtype) <= TOL[dtype]
 
 
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("order", ["rising", "falling"])
+def test_running_max_order(order, dtype, variant):
+    """Keys whose logits against every landmark rise (or fall) along the
+    window: the row maximum m_U is reached in the last (or first) key tile, so
+    a one-pass kernel rescales its partial sums at every tile (or never)."""
+    nw, h, N, d, m = 2, 2, 256, 30, 32
+    need_variant(N, d, m, dtype, variant)
+    q, k, v = W.iid((nw, h, N, d), seed=7 + len(order), dtype=dtype)
+    u = np.abs(q).mean(axis=2, keepdims=True)              # a direction Q-bar agrees with
+    ramp = np.linspace(-1.0, 1.0, N)[None, None, :, None]
+    if order == "falling":
+        ramp = ramp[:, :, ::-1]
+    k = W.round_to(k + 3.0 * ramp * np.sign(q.mean(axis=2, keepdims=True)) * (u > 0), dtype)
+    ref = oracle.forward(q, k, v, m, iters=6, mode=0)
+    got = run(q, k, v, m, dtype, variant)
+    assert error(got, ref, dtype, storage_floor=True) <= TOL[dtype]
+
+
 # --------------------------------------------------------- behaviour ----
 
 def test_deterministic_and_stream_independent():
