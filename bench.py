@@ -37,6 +37,13 @@ def parse():
     ap.add_argument("--no-exact", action="store_true", help="skip the exact-attention timing")
     ap.add_argument("--no-alt", action="store_true", help="skip the other-dtype run")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the benchmark line: time PnP-Nystra and exact attention "
+                         "over N x m x K on the smooth-field recipe and report the error "
+                         "against exact attention (one JSON line per point)")
+    ap.add_argument("--sweep-n", default="64,256,1024,4096")
+    ap.add_argument("--sweep-m", default="8,16,32,64")
+    ap.add_argument("--sweep-k", default="1,3,4,5,6")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="also run a plain device-to-device copy of this many MiB (3 times), "
                          "the reference kernel for scaling HBM byte counters")
@@ -148,6 +155,69 @@ def cpu_baseline(wl, q, k, v, budget_s):
                       f"oracle, {dt:.1f} s wall"}
 
 
+def sweep(args):
+    """(m, K, N) sweep on the c4-style smooth field: a 512x512x180 map (6 heads,
+    d_h = 30) cut into windows of N tokens, so the number of units falls as N
+    grows (24576 units at N = 64 ... 384 at N = 4096).  Per point: kernel times
+    of PnP-Nystra and of exact attention (one event pair around back-to-back
+    launches on the same buffers) and the error of PnP-Nystra against exact
+    attention over all outputs (relative RMS and max-abs)."""
+    import torch
+    from paper_2506_08520_amd import binding as B
+    from paper_2506_08520_amd import workloads as W
+
+    B.lib()
+    base = W.CONFIGS["c4"]
+    side, heads, d = 512, base.heads, base.d
+
+    def timed(fn, reps):
+        s = torch.cuda.current_stream()
+        fn()
+        r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        r0.record(s)
+        for _ in range(reps):
+            fn()
+        r1.record(s)
+        torch.cuda.synchronize()
+        return r0.elapsed_time(r1) / reps
+
+    for N in (int(x) for x in args.sweep_n.split(",")):
+        w = int(round(N ** 0.5))
+        wl = W.Workload(f"sweep-N{N}", (side // w) ** 2, heads, N, d, base.m, ("f32",), "smooth",
+                        base.seed, f"smooth field {side}x{side}x{heads * d}, {w}x{w} windows")
+        q, k, v = (torch.from_numpy(x).float().cuda() for x in W.generate(wl, "f32"))
+        for dt in (args.dtype,):
+            tdt = torch.float32 if dt == "f32" else torch.bfloat16
+            tq, tk, tv = (x.to(tdt) for x in (q, k, v))
+            ex = torch.empty_like(tq)
+            reps = max(3, min(50, int(2e5 // (wl.units * N / 64))))
+            t_ex = timed(lambda: B.nystra_exact_attn_forward(tq, tk, tv, out=ex), reps)
+            exf = ex.float()
+            ref_rms = float(exf.pow(2).mean().sqrt())
+            for m in (int(x) for x in args.sweep_m.split(",")):
+                if m > N:
+                    continue
+                for K in (int(x) for x in args.sweep_k.split(",")):
+                    o = torch.empty_like(tq)
+                    opts = B.make_opts(pinv_iters=K)
+                    t = timed(lambda: B.nystra_attn_forward_ex(tq, tk, tv, m, opts=opts, out=o),
+                              reps)
+                    diff = (o.float() - exf)
+                    print(json.dumps({
+                        "N": N, "m": m, "K": K, "dtype": dt, "units": wl.units,
+                        "variant": "mfma-tiled" if B.nystra_select_variant(
+                            N, d, m, B.F32 if dt == "f32" else B.BF16,
+                            B.make_opts(pinv_iters=K)) == 2 else "generic",
+                        "nystra_us": round(t * 1e3, 2), "exact_us": round(t_ex * 1e3, 2),
+                        "speedup_vs_exact": round(t_ex / t, 3),
+                        "rel_rms_err_vs_exact": float(diff.pow(2).mean().sqrt()) / ref_rms,
+                        "max_abs_err_vs_exact": float(diff.abs().max())}), flush=True)
+        del q, k, v, tq, tk, tv, ex
+        torch.cuda.empty_cache()
+    return 0
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -155,6 +225,8 @@ def main():
               "(window, head) units are independent, so N GPUs would each run 1/N of the "
               "windows with no communication.", file=sys.stderr)
         return 2
+    if args.sweep:
+        return sweep(args)
     import torch
     from paper_2506_08520_amd import binding as B
     from paper_2506_08520_amd import workloads as W

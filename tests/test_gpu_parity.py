@@ -243,6 +243,24 @@ def test_running_max_order(order, dtype, variant):
     assert error(got, ref, dtype, storage_floor=True) <= TOL[dtype]
 
 
+# (m, K, N) grid of the sweep mode of bench.py, on small maps of its recipe
+# (smooth field, d_h = 30): every (N, m) at K = 4 and the corners at other K.
+SWEEP = ([(N, m, 4) for N in (64, 256, 1024, 4096) for m in (8, 16, 32, 64) if m <= N] +
+         [(N, m, K) for N, m in ((64, 8), (4096, 64)) for K in (1, 3, 5, 6)])
+
+
+@pytest.mark.parametrize("N,m,K", SWEEP)
+def test_sweep_grid(N, m, K):
+    w = int(round(N ** 0.5))
+    wl = W.Workload("sweep", 4, 2, N, 30, m, ("f32",), "smooth", 2000 + N, f"{w}x{w} windows")
+    q, k, v = W.generate(wl, "f32")
+    ref = oracle.forward(q, k, v, m, iters=K, mode=0)
+    got = run(q, k, v, m, "f32", B.VARIANT_AUTO, iters=K)
+    err = error(got, ref, "f32")
+    print(f"N={N} m={m} K={K}: max-abs {err:.3e}")
+    assert err <= TOL["f32"]
+
+
 # --------------------------------------------------------- behaviour ----
 
 def test_deterministic_and_stream_independent():
