@@ -27,7 +27,7 @@
  *   is a valid no-op (pointers may then be NULL).  NYSTRA_ERR_HIP reports a
  *   failed launch; nystra_last_error() then holds the HIP message for the
  *   calling thread.  Nothing throws or aborts across this boundary.
- * Limits.  1 <= N <= 4096, 1 <= d_h <= 64, 1 <= m <= min(N, 64),
+ * Limits.  1 <= N <= 2^20, 1 <= d_h <= 64, 1 <= m <= min(N, 64),
  *   n_windows * heads <= 2^31 - 1, 0 <= pinv_iters <= 64.  Pointers must be
  *   aligned to the element size.  O must not overlap Q, K or V (Q, K, V may
  *   alias each other).

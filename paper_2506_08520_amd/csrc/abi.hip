@@ -44,7 +44,9 @@ using nystra::Problem;
 
 namespace {
 
-constexpr int kMaxN = 4096;
+// Tokens per window: up to 2^20 (a 1024 x 1024 map as one global window).  The
+// kernels stream over tokens with 64-bit offsets and size LDS independently of N.
+constexpr int kMaxN = 1 << 20;
 constexpr int kMaxD = 64;
 constexpr int kMaxM = 64;
 constexpr int kMaxIters = 64;

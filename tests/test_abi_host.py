@@ -86,7 +86,7 @@ def fwd(L, q=P, k=P + (1 << 24), v=P + (2 << 24), o=P + (3 << 24), W=2, H=3, N=6
 def test_forward_validation(L):
     assert fwd(L, dtype=2) == EDTYPE
     assert fwd(L, dtype=-1) == EDTYPE
-    for kw in [dict(N=0), dict(N=4097), dict(d=0), dict(d=65), dict(m=0), dict(m=65, N=4096),
+    for kw in [dict(N=0), dict(N=(1 << 20) + 1), dict(d=0), dict(d=65), dict(m=0), dict(m=65, N=4096),
                dict(m=65), dict(W=-1), dict(H=-2), dict(N=63, m=7), dict(N=64, m=3),
                dict(W=1 << 16, H=1 << 16)]:
         assert fwd(L, **kw) == ESHAPE, kw

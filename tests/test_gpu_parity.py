@@ -261,6 +261,31 @@ def test_sweep_grid(N, m, K):
     assert err <= TOL["f32"]
 
 
+# One window covering a whole map (global attention with pooled landmarks):
+# (heads, N, d, m, mode, dtype).  d = 20 has no tiled kernel.
+GLOBAL = [(2, 16384, 32, 64, 0, "f32"), (2, 16384, 32, 16, 1, "f32"), (1, 16384, 20, 64, 0, "f32"),
+          (2, 65536, 32, 64, 0, "f32"), (2, 65536, 32, 64, 0, "bf16"), (2, 16384, 30, 32, 0, "bf16")]
+
+
+@pytest.mark.parametrize("shape", GLOBAL, ids=lambda s: "x".join(map(str, s)))
+def test_global_window(shape):
+    h, N, d, m, mode, dtype = shape
+    q, k, v = W.iid((1, h, N, d), seed=N + d + m + mode, dtype=dtype)
+    ref = oracle.forward(q, k, v, m, iters=6, mode=mode)
+    got = run(q, k, v, m, dtype, B.VARIANT_AUTO, mode=mode)
+    err = error(got, ref, dtype)
+    print(f"N={N} d={d} m={m} mode={mode} {dtype}: error {err:.3e}")
+    assert err <= TOL[dtype]
+
+
+def test_exact_kernel_long_window():
+    """Exact attention at N = 8192 (V^T no longer fits the LDS stage)."""
+    q, k, v = W.iid((1, 1, 8192, 32), seed=8192, dtype="f32")
+    ref = oracle.exact(q, k, v)
+    got = to_host(B.nystra_exact_attn_forward(*(to_dev(x, "f32") for x in (q, k, v))))
+    assert error(got, ref, "f32") <= TOL["f32"]
+
+
 # --------------------------------------------------------- behaviour ----
 
 def test_deterministic_and_stream_independent():
