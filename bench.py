@@ -44,6 +44,8 @@ def parse():
     ap.add_argument("--sweep-n", default="64,256,1024,4096")
     ap.add_argument("--sweep-m", default="8,16,32,64")
     ap.add_argument("--sweep-k", default="1,3,4,5,6")
+    ap.add_argument("--sweep-side", type=int, default=512,
+                    help="side of the square feature map the sweep cuts into windows")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="also run a plain device-to-device copy of this many MiB (3 times), "
                          "the reference kernel for scaling HBM byte counters")
@@ -156,19 +158,22 @@ def cpu_baseline(wl, q, k, v, budget_s):
 
 
 def sweep(args):
-    """(m, K, N) sweep on the c4-style smooth field: a 512x512x180 map (6 heads,
-    d_h = 30) cut into windows of N tokens, so the number of units falls as N
-    grows (24576 units at N = 64 ... 384 at N = 4096).  Per point: kernel times
-    of PnP-Nystra and of exact attention (one event pair around back-to-back
-    launches on the same buffers) and the error of PnP-Nystra against exact
-    attention over all outputs (relative RMS and max-abs)."""
+    """(m, K, N) sweep on the c4-style smooth field: a side x side x 180 map
+    (6 heads, d_h = 30; side 512 by default) cut into windows of N tokens, so
+    the number of units falls as N grows (24576 units at N = 64 ... 6 at
+    N = 262144, one window per map).  Per point: kernel times (one event pair
+    around back-to-back launches on the same buffers) of the one-pass kernels
+    (nystra_attn_forward_ex), of the token-split kernels (forced, through
+    nystra_attn_forward_ws, where they cover the shape), of the automatic
+    choice of nystra_attn_forward_ws and of exact attention, and the error of
+    that choice against exact attention over all outputs."""
     import torch
     from paper_2506_08520_amd import binding as B
     from paper_2506_08520_amd import workloads as W
 
     B.lib()
     base = W.CONFIGS["c4"]
-    side, heads, d = 512, base.heads, base.d
+    side, heads, d = args.sweep_side, base.heads, base.d
 
     def timed(fn, reps):
         s = torch.cuda.current_stream()
@@ -182,12 +187,15 @@ def sweep(args):
         torch.cuda.synchronize()
         return r0.elapsed_time(r1) / reps
 
+    names = {B.VARIANT_GENERIC: "generic", B.VARIANT_TILED: "mfma-tiled",
+             B.VARIANT_SPLIT: "token-split"}
     for N in (int(x) for x in args.sweep_n.split(",")):
         w = int(round(N ** 0.5))
         wl = W.Workload(f"sweep-N{N}", (side // w) ** 2, heads, N, d, base.m, ("f32",), "smooth",
                         base.seed, f"smooth field {side}x{side}x{heads * d}, {w}x{w} windows")
         q, k, v = (torch.from_numpy(x).float().cuda() for x in W.generate(wl, "f32"))
         for dt in (args.dtype,):
+            code = B.F32 if dt == "f32" else B.BF16
             tdt = torch.float32 if dt == "f32" else torch.bfloat16
             tq, tk, tv = (x.to(tdt) for x in (q, k, v))
             ex = torch.empty_like(tq)
@@ -201,18 +209,37 @@ def sweep(args):
                 for K in (int(x) for x in args.sweep_k.split(",")):
                     o = torch.empty_like(tq)
                     opts = B.make_opts(pinv_iters=K)
-                    t = timed(lambda: B.nystra_attn_forward_ex(tq, tk, tv, m, opts=opts, out=o),
-                              reps)
+                    t1 = timed(lambda: B.nystra_attn_forward_ex(tq, tk, tv, m, opts=opts, out=o),
+                               reps)
+                    sopts = B.make_opts(pinv_iters=K, variant=B.VARIANT_SPLIT)
+                    t_split = None
+                    try:
+                        nb = B.nystra_attn_workspace_size(wl.n_windows, heads, N, d, m, code,
+                                                          sopts)
+                    except B.NystraError:
+                        nb = 0
+                    if nb:
+                        wsb = torch.empty(nb, dtype=torch.uint8, device="cuda")
+                        t_split = timed(lambda: B.nystra_attn_forward_ws(
+                            tq, tk, tv, m, opts=sopts, workspace=wsb, out=o), reps)
+                        del wsb
+                    na = B.nystra_attn_workspace_size(wl.n_windows, heads, N, d, m, code, opts)
+                    wsa = torch.empty(max(na, 1), dtype=torch.uint8, device="cuda")
+                    t = timed(lambda: B.nystra_attn_forward_ws(tq, tk, tv, m, opts=opts,
+                                                               workspace=wsa, out=o), reps)
                     diff = (o.float() - exf)
+                    one = names[B.nystra_select_variant(N, d, m, code, opts)]
                     print(json.dumps({
                         "N": N, "m": m, "K": K, "dtype": dt, "units": wl.units,
-                        "variant": "mfma-tiled" if B.nystra_select_variant(
-                            N, d, m, B.F32 if dt == "f32" else B.BF16,
-                            B.make_opts(pinv_iters=K)) == 2 else "generic",
-                        "nystra_us": round(t * 1e3, 2), "exact_us": round(t_ex * 1e3, 2),
+                        "variant": "token-split" if na else one,
+                        "nystra_us": round(t * 1e3, 2), "onepass_variant": one,
+                        "onepass_us": round(t1 * 1e3, 2),
+                        "split_us": round(t_split * 1e3, 2) if t_split else None,
+                        "exact_us": round(t_ex * 1e3, 2),
                         "speedup_vs_exact": round(t_ex / t, 3),
                         "rel_rms_err_vs_exact": float(diff.pow(2).mean().sqrt()) / ref_rms,
                         "max_abs_err_vs_exact": float(diff.abs().max())}), flush=True)
+                    del wsa
         del q, k, v, tq, tk, tv, ex
         torch.cuda.empty_cache()
     return 0

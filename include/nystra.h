@@ -35,6 +35,7 @@
 #ifndef NYSTRA_H
 #define NYSTRA_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -54,15 +55,18 @@ typedef enum { NYSTRA_F32 = 0, NYSTRA_BF16 = 1 } nystra_dtype;
  *  NYSTRA_LM_SEGMENT1D: m contiguous runs of N/m tokens (requires m | N). */
 typedef enum { NYSTRA_LM_POOL2D = 0, NYSTRA_LM_SEGMENT1D = 1 } nystra_landmark_mode;
 
-/* Kernel family used by nystra_attn_forward_ex.  AUTO picks the MFMA-tiled
+/* Kernel family.  AUTO picks, for nystra_attn_forward_ex, the MFMA-tiled
  * kernel when the shape is one it covers and the pointers are aligned as it
  * needs (V and O to 16 bytes; for bf16 also Q and K to 4 bytes), and the
- * generic kernel otherwise; the other values force one
- * (NYSTRA_ERR_UNSUPPORTED if it cannot run). */
+ * generic kernel otherwise; nystra_attn_forward_ws may in addition pick the
+ * token-split kernels (see there).  The other values force one
+ * (NYSTRA_ERR_UNSUPPORTED if it cannot run this shape, or -- for SPLIT -- if
+ * the entry point takes no workspace). */
 typedef enum {
     NYSTRA_VARIANT_AUTO = 0,
     NYSTRA_VARIANT_GENERIC = 1,
-    NYSTRA_VARIANT_TILED = 2
+    NYSTRA_VARIANT_TILED = 2,
+    NYSTRA_VARIANT_SPLIT = 3
 } nystra_variant;
 
 typedef enum {
@@ -74,7 +78,8 @@ typedef enum {
     NYSTRA_ERR_OVERLAP = 5,     /* O overlaps Q, K or V                        */
     NYSTRA_ERR_UNSUPPORTED = 6, /* forced variant cannot run this shape        */
     NYSTRA_ERR_HIP = 7,         /* kernel launch failed (see nystra_last_error) */
-    NYSTRA_ERR_ARG = 8          /* other bad argument (mode, iters, scale)     */
+    NYSTRA_ERR_ARG = 8,         /* other bad argument (mode, iters, scale)     */
+    NYSTRA_ERR_WORKSPACE = 9    /* workspace missing, too small or misaligned  */
 } nystra_status;
 
 typedef struct nystra_opts {
@@ -109,6 +114,39 @@ int nystra_attn_forward_ex(const void *Q, const void *K, const void *V, void *O,
                            int n_windows, int heads, int N, int d_h, int m, int dtype,
                            const nystra_opts *opts, void *stream);
 
+/* Token-split PnP-Nystra for windows with many tokens and few units (global
+ * attention: one window per feature map, N up to 2^20).  The same
+ * computation as nystra_attn_forward_ex (Algorithm 1, Eq. (8)), organised as
+ * six launches on `stream` so that every pass has thousands of workgroups:
+ * landmark pooling in patch pieces (Step 1); per key chunk the row maxima of
+ * S_U over the chunk and G_U^n [V | 1] against them; the chunk results merged
+ * against the global row maxima m_U (Step 3, G_U side -- the sums are those of
+ * the one-pass form, only added in another order); the landmark core per unit
+ * (Steps 2, 4, 5-6); and per query chunk Steps 3 (G_L side), 6 and 7.
+ *
+ * nystra_attn_workspace_size stores in *bytes the device workspace that
+ * nystra_attn_forward_ws needs for these arguments: 0 unless the call would
+ * run the token-split kernels.  AUTO chooses them when the shape is supported
+ * (N % 16 == 0, d_h in {8, 16, 24, 30, 32}, m <= 64; for bf16, Q, K, V 4-byte
+ * aligned) and the units are too few for one workgroup per unit to fill the
+ * GPU; NYSTRA_VARIANT_SPLIT forces them.  The size depends on the arguments
+ * only, not on any pointer (aligned tensors are assumed), and is about
+ * units x (N / chunk) x 8.7 KB for key chunks of 256..4096 tokens.  Host-only.
+ *
+ * nystra_attn_forward_ws: as nystra_attn_forward_ex, with `workspace` a
+ * caller-owned DEVICE buffer of at least the size above, 256-byte aligned and
+ * disjoint from Q, K, V and O (NYSTRA_ERR_WORKSPACE otherwise; it may be NULL
+ * when the size is 0).  Its contents on entry do not matter and on return are
+ * unspecified; calls that may run concurrently need distinct workspaces.
+ * Nothing is allocated. */
+int nystra_attn_workspace_size(int n_windows, int heads, int N, int d_h, int m, int dtype,
+                               const nystra_opts *opts, size_t *bytes);
+
+int nystra_attn_forward_ws(const void *Q, const void *K, const void *V, void *O,
+                           int n_windows, int heads, int N, int d_h, int m, int dtype,
+                           const nystra_opts *opts, void *workspace, size_t workspace_bytes,
+                           void *stream);
+
 /* Exact windowed softmax self-attention, Eq. (1), per unit:
  *   O = softmax(scale Q K^T) V, with the row maximum subtracted inside the
  *   softmax.  scale <= 0 selects 1/sqrt(d_h).  Same layout, limits and
@@ -131,7 +169,8 @@ int nystra_landmark_map(int N, int m, int mode, int32_t *map_host);
 /* Host-only: which kernel family nystra_attn_forward_ex would launch for
  * this shape and options with 16-byte aligned tensors (NYSTRA_VARIANT_GENERIC
  * or NYSTRA_VARIANT_TILED), or a negative nystra_status if the arguments are
- * invalid. */
+ * invalid (NYSTRA_VARIANT_SPLIT, which needs a workspace, gives
+ * -NYSTRA_ERR_UNSUPPORTED). */
 int nystra_select_variant(int N, int d_h, int m, int dtype, const nystra_opts *opts);
 
 /* Static description of a status code. */

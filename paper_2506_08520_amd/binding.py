@@ -15,13 +15,14 @@ LIB_PATH = os.path.join(_HERE, "libnystra.so")
 
 F32, BF16 = 0, 1
 LM_POOL2D, LM_SEGMENT1D = 0, 1
-VARIANT_AUTO, VARIANT_GENERIC, VARIANT_TILED = 0, 1, 2
+VARIANT_AUTO, VARIANT_GENERIC, VARIANT_TILED, VARIANT_SPLIT = 0, 1, 2, 3
 
 # Every symbol the header declares.
 EXPORTS = (
     "nystra_default_opts", "nystra_attn_forward", "nystra_attn_forward_ex",
     "nystra_exact_attn_forward", "nystra_landmark_pool", "nystra_landmark_map",
-    "nystra_select_variant", "nystra_status_str", "nystra_last_error",
+    "nystra_select_variant", "nystra_attn_workspace_size", "nystra_attn_forward_ws",
+    "nystra_status_str", "nystra_last_error",
 )
 
 
@@ -62,11 +63,15 @@ def lib():
     L.nystra_landmark_pool.argtypes = [_vp] * 5 + [_i] * 7 + [_vp]
     L.nystra_landmark_map.argtypes = [_i, _i, _i, _vp]
     L.nystra_select_variant.argtypes = [_i, _i, _i, _i, ctypes.POINTER(Opts)]
+    L.nystra_attn_workspace_size.argtypes = [_i] * 6 + [ctypes.POINTER(Opts),
+                                                         ctypes.POINTER(ctypes.c_size_t)]
+    L.nystra_attn_forward_ws.argtypes = ([_vp] * 4 + [_i] * 6 +
+                                         [ctypes.POINTER(Opts), _vp, ctypes.c_size_t, _vp])
     L.nystra_status_str.argtypes = [_i]
     L.nystra_status_str.restype = ctypes.c_char_p
     L.nystra_last_error.argtypes = []
     L.nystra_last_error.restype = ctypes.c_char_p
-    for name in EXPORTS[:7]:
+    for name in EXPORTS[:9]:
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -135,6 +140,34 @@ def nystra_attn_forward_ex(q, k, v, m, opts=None, out=None, stream=None):
     rc = lib().nystra_attn_forward_ex(_ptr(q), _ptr(k), _ptr(v), _ptr(o), W, H, N, d, m,
                                       _dtype_code(q), po, _stream(stream))
     _check(rc, "nystra_attn_forward_ex")
+    return o
+
+
+def nystra_attn_workspace_size(n_windows, heads, N, d_h, m, dtype=F32, opts=None):
+    """Bytes of device workspace nystra_attn_forward_ws needs (0: none)."""
+    n = ctypes.c_size_t(0)
+    po = ctypes.byref(opts) if opts is not None else None
+    _check(lib().nystra_attn_workspace_size(n_windows, heads, N, d_h, m, dtype, po,
+                                            ctypes.byref(n)), "nystra_attn_workspace_size")
+    return int(n.value)
+
+
+def nystra_attn_forward_ws(q, k, v, m, opts=None, workspace=None, out=None, stream=None):
+    """PnP-Nystra through the workspace entry point.  `workspace` is a device
+    tensor of at least nystra_attn_workspace_size() bytes; when None, one of
+    exactly that size is allocated from torch's allocator (256-byte aligned)."""
+    import torch
+    W, H, N, d = _shape(q, k, v)
+    code = _dtype_code(q)
+    o = torch.empty_like(q) if out is None else out
+    need = nystra_attn_workspace_size(W, H, N, d, m, code, opts)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    po = ctypes.byref(opts) if opts is not None else None
+    rc = lib().nystra_attn_forward_ws(_ptr(q), _ptr(k), _ptr(v), _ptr(o), W, H, N, d, m, code,
+                                      po, _ptr(workspace), nbytes, _stream(stream))
+    _check(rc, "nystra_attn_forward_ws")
     return o
 
 

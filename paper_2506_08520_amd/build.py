@@ -9,7 +9,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libnystra.so")
 OBJDIR = os.path.join(os.path.dirname(HERE), "_build")
-SOURCES = ["abi.hip", "generic.hip", "exact.hip", "tiled.hip", "tiled_large.hip"]
+SOURCES = ["abi.hip", "generic.hip", "exact.hip", "tiled.hip", "tiled_large.hip",
+           "split.hip"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -107,10 +107,16 @@ int finish_launch(hipError_t e)
     return NYSTRA_OK;
 }
 
-// Resolves options and the problem; does not touch device memory.
+// Token-split kernels pay off when one workgroup per unit would leave the GPU
+// short of work: few units with long windows.
+bool split_preferred(const Problem &p) { return p.units < 512 && p.N >= 2048; }
+
+// Resolves options and the problem; does not touch device memory.  with_ws
+// says whether the entry point takes a workspace (and so may run the
+// token-split kernels).
 int build_problem(const void *Q, const void *K, const void *V, void *O, int n_windows,
                   int heads, int N, int d, int m, int dtype, const nystra_opts *opts,
-                  Problem *p, int *variant)
+                  bool with_ws, Problem *p, int *variant)
 {
     nystra_opts o;
     nystra_default_opts(&o);
@@ -124,7 +130,7 @@ int build_problem(const void *Q, const void *K, const void *V, void *O, int n_wi
         return NYSTRA_ERR_SHAPE;
     if (o.pinv_iters < 0 || o.pinv_iters > kMaxIters || !isfinite(o.scale) ||
         (o.landmark_mode != NYSTRA_LM_POOL2D && o.landmark_mode != NYSTRA_LM_SEGMENT1D) ||
-        o.variant < NYSTRA_VARIANT_AUTO || o.variant > NYSTRA_VARIANT_TILED)
+        o.variant < NYSTRA_VARIANT_AUTO || o.variant > NYSTRA_VARIANT_SPLIT)
         return NYSTRA_ERR_ARG;
     nystra::Geometry g;
     if (!nystra::make_geometry(N, m, o.landmark_mode, &g))
@@ -142,11 +148,23 @@ int build_problem(const void *Q, const void *K, const void *V, void *O, int n_wi
     p->scale = o.scale > 0.f ? o.scale : float(1.0 / sqrt(double(d)));
     p->geo = g;
     const bool tiled = nystra::tiled_supported(*p);
-    if (o.variant == NYSTRA_VARIANT_TILED && !tiled)
-        return NYSTRA_ERR_UNSUPPORTED;
-    *variant = (o.variant == NYSTRA_VARIANT_GENERIC || !tiled) ? NYSTRA_VARIANT_GENERIC
-                                                               : NYSTRA_VARIANT_TILED;
-    return NYSTRA_OK;
+    const bool split = with_ws && nystra::split_supported(*p);
+    switch (o.variant) {
+    case NYSTRA_VARIANT_GENERIC:
+        *variant = NYSTRA_VARIANT_GENERIC;
+        return NYSTRA_OK;
+    case NYSTRA_VARIANT_TILED:
+        *variant = NYSTRA_VARIANT_TILED;
+        return tiled ? NYSTRA_OK : NYSTRA_ERR_UNSUPPORTED;
+    case NYSTRA_VARIANT_SPLIT:
+        *variant = NYSTRA_VARIANT_SPLIT;
+        return split ? NYSTRA_OK : NYSTRA_ERR_UNSUPPORTED;
+    default:
+        *variant = (split && split_preferred(*p)) ? NYSTRA_VARIANT_SPLIT
+                   : tiled                        ? NYSTRA_VARIANT_TILED
+                                                  : NYSTRA_VARIANT_GENERIC;
+        return NYSTRA_OK;
+    }
 }
 
 }  // namespace
@@ -170,7 +188,8 @@ int nystra_attn_forward_ex(const void *Q, const void *K, const void *V, void *O,
 {
     Problem p;
     int variant = 0;
-    int rc = build_problem(Q, K, V, O, n_windows, heads, N, d_h, m, dtype, opts, &p, &variant);
+    int rc = build_problem(Q, K, V, O, n_windows, heads, N, d_h, m, dtype, opts, false, &p,
+                           &variant);
     if (rc != NYSTRA_OK)
         return rc;
     if (p.units == 0)
@@ -180,6 +199,55 @@ int nystra_attn_forward_ex(const void *Q, const void *K, const void *V, void *O,
     if (rc != NYSTRA_OK)
         return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    if (variant == NYSTRA_VARIANT_TILED)
+        return finish_launch(nystra::launch_tiled_forward(p, s));
+    return finish_launch(nystra::launch_generic_forward(p, s));
+}
+
+int nystra_attn_workspace_size(int n_windows, int heads, int N, int d_h, int m, int dtype,
+                               const nystra_opts *opts, size_t *bytes)
+{
+    if (!bytes)
+        return NYSTRA_ERR_NULL;
+    Problem p;
+    int variant = 0;
+    int rc = build_problem(nullptr, nullptr, nullptr, nullptr, n_windows, heads, N, d_h, m,
+                           dtype, opts, true, &p, &variant);
+    if (rc != NYSTRA_OK)
+        return rc;
+    *bytes = (variant == NYSTRA_VARIANT_SPLIT && p.units > 0)
+                 ? nystra::split_workspace_bytes(p) : 0;
+    return NYSTRA_OK;
+}
+
+int nystra_attn_forward_ws(const void *Q, const void *K, const void *V, void *O,
+                           int n_windows, int heads, int N, int d_h, int m, int dtype,
+                           const nystra_opts *opts, void *workspace, size_t workspace_bytes,
+                           void *stream)
+{
+    Problem p;
+    int variant = 0;
+    int rc = build_problem(Q, K, V, O, n_windows, heads, N, d_h, m, dtype, opts, true, &p,
+                           &variant);
+    if (rc != NYSTRA_OK)
+        return rc;
+    if (p.units == 0)
+        return NYSTRA_OK;
+    const int64_t bytes = p.units * N * d_h * dtype_bytes(dtype);
+    rc = check_tensors(Q, K, V, O, bytes, dtype_bytes(dtype));
+    if (rc != NYSTRA_OK)
+        return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (variant == NYSTRA_VARIANT_SPLIT) {
+        const size_t need = nystra::split_workspace_bytes(p);
+        if (!workspace || workspace_bytes < need || misaligned(workspace, 256))
+            return NYSTRA_ERR_WORKSPACE;
+        const int64_t wn = int64_t(need);
+        if (overlaps(workspace, wn, Q, bytes) || overlaps(workspace, wn, K, bytes) ||
+            overlaps(workspace, wn, V, bytes) || overlaps(workspace, wn, O, bytes))
+            return NYSTRA_ERR_WORKSPACE;
+        return finish_launch(nystra::launch_split(p, workspace, s));
+    }
     if (variant == NYSTRA_VARIANT_TILED)
         return finish_launch(nystra::launch_tiled_forward(p, s));
     return finish_launch(nystra::launch_generic_forward(p, s));
@@ -285,8 +353,8 @@ int nystra_select_variant(int N, int d_h, int m, int dtype, const nystra_opts *o
 {
     Problem p;
     int variant = 0;
-    int rc = build_problem(nullptr, nullptr, nullptr, nullptr, 1, 1, N, d_h, m, dtype, opts, &p,
-                           &variant);
+    int rc = build_problem(nullptr, nullptr, nullptr, nullptr, 1, 1, N, d_h, m, dtype, opts,
+                           false, &p, &variant);
     return rc == NYSTRA_OK ? variant : -rc;
 }
 
@@ -302,6 +370,7 @@ const char *nystra_status_str(int status)
     case NYSTRA_ERR_UNSUPPORTED: return "forced kernel variant cannot run this shape";
     case NYSTRA_ERR_HIP: return "HIP launch error";
     case NYSTRA_ERR_ARG: return "invalid argument";
+    case NYSTRA_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
     default: return "unknown status";
     }
 }

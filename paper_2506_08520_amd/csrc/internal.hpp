@@ -44,6 +44,14 @@ hipError_t launch_tiled_forward(const Problem &p, hipStream_t stream);
 bool tiled_large_supported(const Problem &p);
 hipError_t launch_tiled_large(const Problem &p, hipStream_t stream);
 
+// Token-split kernels over a caller-provided workspace (global attention).
+// split_supported() is a host-side test of the shape and pointers;
+// split_workspace_bytes() is the workspace size launch_split() needs, which
+// must be 256-byte aligned.
+bool split_supported(const Problem &p);
+size_t split_workspace_bytes(const Problem &p);
+hipError_t launch_split(const Problem &p, void *workspace, hipStream_t stream);
+
 // Head widths with a tiled instantiation.
 inline bool tiled_width(int d) { return d == 8 || d == 16 || d == 24 || d == 30 || d == 32; }
 

@@ -1,0 +1,735 @@
+// Token-split PnP-Nystra: Algorithm 1 as six launches over a caller-provided
+// workspace, for windows so large, or (window, head) units so few, that one
+// workgroup per unit leaves most of the 256 compute units idle -- global
+// attention, where one window is the whole feature map, is the extreme case.
+//
+//   A   pool     grid units x m x pieces: sums of Q and K over one piece of
+//                one landmark's pooling patch (Step 1).
+//   A2  bar      grid units: Qbar, Kbar = piece sums / patch size.
+//   B   keys     grid units x key chunks: per chunk and landmark, the maximum
+//                of S_U over the chunk's keys and T = G_U [V | 1] against it
+//                (Step 3, G_U side), the four waves merged in LDS.
+//   C   merge    grid units x landmark tiles x 9 column groups: the chunk
+//                records merged to m_U = max over chunks and
+//                T = sum_c exp(s (max_c - m_U)) T_c (same for T_D), the sums
+//                of Step 3 against the global row maximum.
+//   P   core     grid units: Steps 2, 4 and 5-6 (landmark_core).
+//   D   queries  grid units x query chunks: Steps 3 (G_L side), 6 and 7.
+//
+// Only the order of the additions differs from the one-pass kernels.  Q is
+// read twice (A, D), K twice (A, B), V once; O is written once.  Every
+// contraction of B and D runs on the matrix cores exactly as in the one-pass
+// large kernel (fp32, or bf16 with hi + lo terms for bf16 inputs).
+#include "internal.hpp"
+#include "core_tiles.hpp"
+
+namespace nystra {
+namespace {
+
+using namespace tile;
+using namespace core;
+
+constexpr int kWP = 32;                    // pitch (floats) of feature rows in the workspace
+constexpr int kLm = 64;                    // landmark rows reserved per unit
+constexpr int kRecT = kLm * kWP;           // record: T rows, then T_D, then the row maxima
+constexpr int kRecD = kRecT;
+constexpr int kRecM = kRecT + kLm;
+constexpr int kRec = kRecT + 2 * kLm;
+constexpr int kWout = kLm * kTS + kLm;     // W table (pitch kTS) and W_D
+constexpr int kWaves = 4;                  // waves per workgroup of passes A, B, D
+constexpr int kMergeGroups = kWP / 4 + 1;  // column groups of pass C (8 x 4 features, T_D)
+
+struct SplitArgs {
+    int64_t units;
+    int N, d, m, iters;
+    float s2;          // logit scale in base-2 units (scale * log2 e)
+    float inv_patch;   // 1 / tokens per pooling patch
+    int cols, pr, pc, gc;
+    int P;             // tokens per patch
+    int pieces, piece_len;     // pass A: pieces per patch, tokens per piece
+    int nchunk, chunk_len;     // pass B: key chunks per unit, keys per chunk
+    int nqchunk, qchunk_len;   // pass D: query chunks per unit, queries per chunk
+    float *part;   // [units][2][m * pieces][kWP]  piece sums of Q, then K
+    float *bar;    // [units][2][kLm][kWP]         Qbar, then Kbar (zero past m, d)
+    float *rec;    // [units][nchunk][kRec]        chunk records of pass B
+    float *comb;   // [units][kRec]                merged T, T_D and s2 * m_U
+    float *wout;   // [units][kWout]               W and W_D
+};
+
+__device__ inline int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
+// ---- A: piece sums of Q and K ------------------------------------------------
+template <class E, int D>
+__global__ void __launch_bounds__(64 * kWaves)
+split_pool_kernel(const typename E::T *__restrict__ q, const typename E::T *__restrict__ k,
+                  SplitArgs a)
+{
+    __shared__ float red[kWaves][2][4][8];
+    const int per_unit = a.m * a.pieces;
+    const int64_t unit = blockIdx.x / per_unit;
+    const int rem = int(blockIdx.x - unit * per_unit);
+    const int l = rem / a.pieces, r = rem - l * a.pieces;
+    const int i0 = r * a.piece_len, i1 = min(a.P, i0 + a.piece_len);
+    const int w = wave_id(), lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
+    const int r0 = (l / a.gc) * a.pr, c0 = (l % a.gc) * a.pc;
+    const int64_t base = unit * int64_t(a.N) * D;
+    const typename E::T *qu = q + base, *ku = k + base;
+
+    float qs[8], ks[8];
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+        qs[s] = ks[s] = 0.f;
+    // Wave w takes 16-token tiles w, w + 4, ... of the piece; four tiles per
+    // step so that their loads are in flight together.
+    for (int b = i0 + 16 * w; b < i1; b += 4 * 16 * kWaves) {
+        float x[4][8], y[4][8];
+        bool ok[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = b + 16 * kWaves * u + c;
+            ok[u] = i < i1;
+            const int ii = ok[u] ? i : i0;
+            const int64_t t = int64_t(r0 + ii / a.pc) * a.cols + c0 + ii % a.pc;
+            load_chunk8<E, D>(qu + t * D, g, x[u]);
+            load_chunk8<E, D>(ku + t * D, g, y[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (ok[u]) {
+#pragma unroll
+                for (int s = 0; s < 8; ++s) {
+                    qs[s] += x[u][s];
+                    ks[s] += y[u][s];
+                }
+            }
+    }
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+        qs[s] = sum_row(qs[s]);   // every lane of the row holds the sum
+        ks[s] = sum_row(ks[s]);
+    }
+    if (c == 0) {
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+            red[w][0][g][s] = qs[s];
+            red[w][1][g][s] = ks[s];
+        }
+    }
+    __syncthreads();
+    if (w == 0) {
+        // lane (g, c): tensor c >> 3, slot c & 7 of feature group g
+        const int which = c >> 3, s = c & 7;
+        float acc = 0.f;
+#pragma unroll
+        for (int v = 0; v < kWaves; ++v)
+            acc += red[v][which][g][s];
+        if (slot_valid<D>(g, s)) {
+            float *row = a.part + ((unit * 2 + which) * per_unit + rem) * kWP;
+            row[chunk_start<D>(g) + s] = acc;
+        }
+    }
+}
+
+// ---- A2: Qbar and Kbar -----------------------------------------------------
+__global__ void __launch_bounds__(256) split_bar_kernel(SplitArgs a)
+{
+    const int64_t unit = blockIdx.x;
+    const int per_unit = a.m * a.pieces;
+    for (int idx = threadIdx.x; idx < 2 * kLm * kWP; idx += blockDim.x) {
+        const int which = idx / (kLm * kWP), l = (idx / kWP) % kLm, f = idx % kWP;
+        float acc = 0.f;
+        if (l < a.m && f < a.d) {
+            const float *p = a.part + ((unit * 2 + which) * per_unit + l * a.pieces) * kWP + f;
+            for (int r = 0; r < a.pieces; ++r)
+                acc += p[int64_t(r) * kWP];
+            acc *= a.inv_patch;
+        }
+        a.bar[unit * 2 * kLm * kWP + idx] = acc;
+    }
+}
+
+// ---- B: chunk records of the G_U side ----------------------------------------
+template <class E, int MT, int D, bool BFM>
+__global__ void __launch_bounds__(64 * kWaves)
+split_keys_kernel(const typename E::T *__restrict__ k, const typename E::T *__restrict__ v,
+                  SplitArgs a)
+{
+    constexpr int d = D;
+    __shared__ float recs[kWaves][kRec];
+    __shared__ float vecs[kWaves][64];
+    const int64_t unit = blockIdx.x / a.nchunk;
+    const int chunk = int(blockIdx.x - unit * a.nchunk);
+    const int w = wave_id(), lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
+    float *vec = vecs[w];
+    const int m = a.m;
+    const int64_t base = unit * int64_t(a.N) * d;
+    const typename E::T *ku = k + base, *vu = v + base;
+    const uint16_t *ku16 = reinterpret_cast<const uint16_t *>(ku);
+    const uint16_t *vu16 = reinterpret_cast<const uint16_t *>(vu);
+    const float *qbar = a.bar + unit * 2 * kLm * kWP;
+
+    // Qbar rows: lane (g, c) holds landmark 16j + c, the slots of group g.
+    float qb[MT][8];
+    bf8 qbh[MT], qbl[MT];
+#pragma unroll
+    for (int j = 0; j < MT; ++j) {
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+            qb[j][s] = slot_valid<D>(g, s) ? qbar[(16 * j + c) * kWP + chunk_start<D>(g) + s]
+                                           : 0.f;
+        if constexpr (BFM)
+            split_bf16(qb[j], qbh[j], qbl[j]);
+    }
+
+    f4 T[MT][2];
+    float tden[MT], mrun[MT];
+#pragma unroll
+    for (int j = 0; j < MT; ++j) {
+        T[j][0] = T[j][1] = f4{0.f, 0.f, 0.f, 0.f};
+        tden[j] = 0.f;
+        mrun[j] = -INFINITY;
+    }
+    const int k0 = chunk * a.chunk_len, k1 = min(a.N, k0 + a.chunk_len);
+    const int NT = (k1 - k0) >> 4;   // key tiles of the chunk
+    // Wave w takes the tile pairs w, w + 4, ...; the second tile of a pair past
+    // the chunk's end (fp32 path with an odd tile count) repeats the first and
+    // is not accumulated.
+    for (int t0 = 2 * w; t0 < NT; t0 += 2 * kWaves) {
+        float kr[2][8], vr[2][2][4];
+        bf8 kw[2];
+        uint16_t vh[2][2][4];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int tt = min(t0 + u, NT - 1);
+            const int64_t row = int64_t(k0 + 16 * tt + c) * d;
+            if constexpr (BFM)
+                kw[u] = load_chunk8_bf8<D>(ku16 + row, g);
+            else
+                load_chunk8<E, D>(ku + row, g, kr[u]);
+#pragma unroll
+            for (int ct = 0; ct < 2; ++ct) {
+                const int f = 16 * ct + c;
+#pragma unroll
+                for (int s = 0; s < 4; ++s) {
+                    const int64_t idx = int64_t(k0 + 16 * tt + 4 * g + s) * d + min(f, d - 1);
+                    if constexpr (BFM) {
+                        const uint16_t x = vu16[idx];
+                        vh[u][ct][s] = f < d ? x : uint16_t(0);
+                    } else {
+                        const float x = E::load(vu, idx);
+                        vr[u][ct][s] = f < d ? x : 0.f;
+                    }
+                }
+            }
+        }
+        const bool second = t0 + 1 < NT;   // uniform
+#pragma unroll
+        for (int j = 0; j < MT; ++j) {
+            const bool lval = 16 * j + c < m;
+            // S_U^T tiles: lane (g, c) gets S_U[landmark 16j + c][key 16tt + 4g + i].
+            f4 su[2];
+            float gmax = -INFINITY;
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                f4 acc = {0.f, 0.f, 0.f, 0.f};
+                if constexpr (BFM) {
+                    acc = mfma_bf16(kw[u], qbh[j], acc);
+                    acc = mfma_bf16(kw[u], qbl[j], acc);
+                } else {
+#pragma unroll
+                    for (int s = 0; s < 8; ++s)
+                        acc = mfma4(kr[u][s], qb[j][s], acc);
+                }
+                su[u] = acc;
+                gmax = fmaxf(gmax, fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3])));
+            }
+            const float mnew = fmaxf(mrun[j], max_groups(gmax));
+            // Rescale what is accumulated when a maximum grew; the factor is
+            // exactly 1 for every landmark whose maximum held, so skipping the
+            // step when none grew changes nothing.
+            if (__builtin_amdgcn_ballot_w64(mnew != mrun[j]) != 0) {
+                const float f = fast_exp2(a.s2 * (mrun[j] - mnew));
+                tden[j] *= f;
+                const f4 fr = by_rows(f, vec, g, c);   // factor of landmark 16j + 4g + i
+                T[j][0] *= fr;
+                T[j][1] *= fr;
+            }
+            mrun[j] = mnew;
+            const float mb = a.s2 * mnew;
+            if constexpr (BFM) {
+                float gk[8];
+#pragma unroll
+                for (int h = 0; h < 2; ++h)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        gk[4 * h + i] = lval ? fast_exp2(fmaf(a.s2, su[h][i], -mb)) : 0.f;
+                        tden[j] += gk[4 * h + i];
+                    }
+                bf8 gh, gl;
+                split_bf16(gk, gh, gl);
+#pragma unroll
+                for (int ct = 0; ct < 2; ++ct) {
+                    U16B vb;
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj)
+                        vb.w[jj] = uint32_t(vh[jj >> 1][ct][2 * (jj & 1)]) |
+                                   (uint32_t(vh[jj >> 1][ct][2 * (jj & 1) + 1]) << 16);
+                    const bf8 vv = __builtin_bit_cast(bf8, vb);
+                    T[j][ct] = mfma_bf16(gh, vv, T[j][ct]);
+                    T[j][ct] = mfma_bf16(gl, vv, T[j][ct]);
+                }
+            } else {
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    if (u == 1 && !second)
+                        break;
+                    f4 e;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        e[i] = lval ? fast_exp2(fmaf(a.s2, su[u][i], -mb)) : 0.f;
+                        tden[j] += e[i];
+                    }
+#pragma unroll
+                    for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+                        for (int s = 0; s < 4; ++s)
+                            T[j][ct] = mfma4(e[s], vr[u][ct][s], T[j][ct]);
+                }
+            }
+        }
+    }
+
+    // The four waves' records, merged against the largest of their maxima.
+    float *rw = recs[w];
+#pragma unroll
+    for (int j = 0; j < MT; ++j) {
+        const float td = sum_groups(tden[j]);
+#pragma unroll
+        for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                rw[(16 * j + 4 * g + i) * kWP + 16 * ct + c] = T[j][ct][i];
+        if (g == 0) {
+            rw[kRecD + 16 * j + c] = td;
+            rw[kRecM + 16 * j + c] = mrun[j];
+        }
+    }
+    __syncthreads();
+    float *out = a.rec + (unit * a.nchunk + chunk) * kRec;
+    for (int idx = threadIdx.x; idx < 16 * MT * (kWP / 4); idx += 64 * kWaves) {
+        const int l = idx / (kWP / 4), f = 4 * (idx % (kWP / 4));
+        float mx = -INFINITY;
+#pragma unroll
+        for (int v = 0; v < kWaves; ++v)
+            mx = fmaxf(mx, recs[v][kRecM + l]);
+        f4 acc = {0.f, 0.f, 0.f, 0.f};
+        float den = 0.f;
+#pragma unroll
+        for (int v = 0; v < kWaves; ++v) {
+            const float fw = fast_exp2(a.s2 * (recs[v][kRecM + l] - mx));   // 0 for an idle wave
+            acc += fw * *reinterpret_cast<const f4 *>(&recs[v][l * kWP + f]);
+            den += fw * recs[v][kRecD + l];
+        }
+        *reinterpret_cast<f4 *>(out + l * kWP + f) = acc;
+        if (f == 0) {
+            out[kRecD + l] = den;
+            out[kRecM + l] = mx;
+        }
+    }
+}
+
+// ---- C: merge of the chunk records ------------------------------------------
+// Block (unit, landmark tile j, column group q): q < 8 merges features
+// 4q .. 4q+3 of T, q = 8 the column T_D.  Four slices of 64 threads take every
+// fourth chunk; thread (landmark li, column x) of a slice keeps its maximum and
+// sum, and the slices are merged in LDS in a fixed order.  Every block of a
+// tile computes the same maxima (a max is exact), and block q = 0 stores
+// s2 * m_U.
+__global__ void __launch_bounds__(256) split_merge_kernel(SplitArgs a, int MT)
+{
+    __shared__ float smax[4][64], ssum[4][64];
+    const int per_unit = MT * kMergeGroups;
+    const int64_t unit = blockIdx.x / per_unit;
+    const int rem = int(blockIdx.x - unit * per_unit);
+    const int j = rem / kMergeGroups, q = rem - j * kMergeGroups;
+    const int slice = threadIdx.x >> 6, t = threadIdx.x & 63;
+    const int li = t >> 2, x = t & 3;
+    const int l = 16 * j + li;
+    const int col = q < kMergeGroups - 1 ? l * kWP + 4 * q + x : kRecD + l;
+    const float *rec = a.rec + unit * a.nchunk * kRec;
+    float mx = -INFINITY;
+    for (int ch = slice; ch < a.nchunk; ch += 4)
+        mx = fmaxf(mx, rec[int64_t(ch) * kRec + kRecM + l]);
+    float sum = 0.f;
+    for (int ch = slice; ch < a.nchunk; ch += 4) {
+        const float *r = rec + int64_t(ch) * kRec;
+        sum += fast_exp2(a.s2 * (r[kRecM + l] - mx)) * r[col];
+    }
+    smax[slice][t] = mx;
+    ssum[slice][t] = sum;
+    __syncthreads();
+    if (slice == 0) {
+        float M = mx;
+#pragma unroll
+        for (int s = 1; s < 4; ++s)
+            M = fmaxf(M, smax[s][t]);
+        float tot = 0.f;
+#pragma unroll
+        for (int s = 0; s < 4; ++s)   // a slice without chunks has max -inf and weight 0
+            tot += fast_exp2(a.s2 * (smax[s][t] - M)) * ssum[s][t];
+        float *cb = a.comb + unit * kRec;
+        cb[col] = tot;
+        if (q == 0 && x == 0)
+            cb[kRecM + l] = a.s2 * M;
+    }
+}
+
+// ---- P: Steps 2, 4 and 5-6 ---------------------------------------------------
+template <int MT, int D, bool BFM>
+__global__ void __launch_bounds__(64 * MT) split_core_kernel(SplitArgs a)
+{
+    using L = LargeLds<MT>;
+    extern __shared__ float lds[];
+    const int64_t unit = blockIdx.x;
+    const int lt = wave_id(), lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
+    const int l = 16 * lt + c;
+    const float *qbar = a.bar + unit * 2 * kLm * kWP, *kbar = qbar + kLm * kWP;
+    const float *cb = a.comb + unit * kRec;
+    for (int idx = threadIdx.x; idx < 16 * MT * kWP; idx += 64 * MT)
+        lds[L::kbar + (idx / kWP) * kTS + idx % kWP] = kbar[idx];
+    float qb[8];
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+        qb[s] = slot_valid<D>(g, s) ? qbar[l * kWP + chunk_start<D>(g) + s] : 0.f;
+    f4 T[2];
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            T[ct][i] = cb[(16 * lt + 4 * g + i) * kWP + 16 * ct + c];
+    const float tden = cb[kRecD + l], mu = cb[kRecM + l];
+    __syncthreads();   // Kbar in LDS
+    landmark_core<MT, D, BFM>(lds, qb, mu, T, tden, a.m, a.iters, a.s2, lt, lane);
+    float *wo = a.wout + unit * kWout;
+    for (int idx = threadIdx.x; idx < table_den<MT>() + 16 * MT; idx += 64 * MT)
+        wo[idx] = lds[L::wb + idx];
+}
+
+// ---- D: Steps 3 (G_L side), 6 and 7 -----------------------------------------
+template <class E, int MT, int D, bool BFM>
+__global__ void __launch_bounds__(64 * kWaves)
+split_query_kernel(const typename E::T *__restrict__ q, typename E::T *__restrict__ o,
+                   SplitArgs a)
+{
+    constexpr int d = D;
+    constexpr int TDo = table_den<MT>();
+    constexpr int MP = (MT + 1) / 2;   // landmark tile pairs (bf16 path)
+    __shared__ float vecs[kWaves][64];
+    const int64_t unit = blockIdx.x / a.nqchunk;
+    const int qc = int(blockIdx.x - unit * a.nqchunk);
+    const int w = wave_id(), lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
+    float *vec = vecs[w];
+    const int m = a.m;
+    const int64_t base = unit * int64_t(a.N) * d;
+    const typename E::T *qu = q + base;
+    typename E::T *ou = o + base;
+    const float *Wb = a.wout + unit * kWout;
+    const float *kbar = a.bar + unit * 2 * kLm * kWP + kLm * kWP;
+
+    f4 WR[MT][2], wdv[MT];
+    float kb[MT][8];
+#pragma unroll
+    for (int kk = 0; kk < MT; ++kk) {
+        WR[kk][0] = read_r<kTS>(Wb, kk, 0, g, c);
+        WR[kk][1] = read_r<kTS>(Wb, kk, 1, g, c);
+        wdv[kk] = *reinterpret_cast<const f4 *>(Wb + TDo + 16 * kk + 4 * g);
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+            kb[kk][s] = slot_valid<D>(g, s) ? kbar[(16 * kk + c) * kWP + chunk_start<D>(g) + s]
+                                            : 0.f;
+    }
+    bf8 kbh[MT], kbl[MT], wh[MP][2], wl[MP][2];
+    if constexpr (BFM) {
+#pragma unroll
+        for (int kk = 0; kk < MT; ++kk)
+            split_bf16(kb[kk], kbh[kk], kbl[kk]);
+#pragma unroll
+        for (int kp = 0; kp < MP; ++kp)
+#pragma unroll
+            for (int ct = 0; ct < 2; ++ct) {
+                float w8[8];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    w8[i] = WR[2 * kp][ct][i];
+                    w8[4 + i] = (2 * kp + 1 < MT) ? WR[(2 * kp + 1) % MT][ct][i] : 0.f;
+                }
+                split_bf16(w8, wh[kp][ct], wl[kp][ct]);
+            }
+    }
+    const uint16_t *qu16 = reinterpret_cast<const uint16_t *>(qu);
+    const int q0 = qc * a.qchunk_len, q1 = min(a.N, q0 + a.qchunk_len);
+    const int NT = (q1 - q0) >> 4;
+    constexpr int kQGroup = 2;
+    for (int t0 = w; t0 < NT; t0 += kQGroup * kWaves) {
+        float qg[kQGroup][8];
+        bf8 qw[kQGroup];
+#pragma unroll
+        for (int u = 0; u < kQGroup; ++u) {
+            const int64_t row = int64_t(q0 + 16 * min(t0 + u * kWaves, NT - 1) + c) * d;
+            if constexpr (BFM)
+                qw[u] = load_chunk8_bf8<D>(qu16 + row, g);
+            else
+                load_chunk8<E, D>(qu + row, g, qg[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < kQGroup; ++u) {
+            const int tt = t0 + u * kWaves;
+            if (tt >= NT)
+                break;   // uniform
+            f4 glT[MT];   // lane (g,c): G_L^n[token 16tt+c][landmark 16kk+4g+i]
+            float ml = -INFINITY;
+#pragma unroll
+            for (int kk = 0; kk < MT; ++kk) {
+                f4 acc = {0.f, 0.f, 0.f, 0.f};
+                if constexpr (BFM) {
+                    acc = mfma_bf16(kbh[kk], qw[u], acc);
+                    acc = mfma_bf16(kbl[kk], qw[u], acc);
+                } else {
+#pragma unroll
+                    for (int s = 0; s < 8; ++s)
+                        acc = mfma4(kb[kk][s], qg[u][s], acc);
+                }
+                glT[kk] = acc;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (16 * kk + 4 * g + i < m)
+                        ml = fmaxf(ml, acc[i]);
+            }
+            ml = a.s2 * max_groups(ml);
+            float od = 0.f;
+#pragma unroll
+            for (int kk = 0; kk < MT; ++kk)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float e = (16 * kk + 4 * g + i < m)
+                                        ? fast_exp2(fmaf(a.s2, glT[kk][i], -ml)) : 0.f;
+                    glT[kk][i] = e;
+                    od = fmaf(e, wdv[kk][i], od);
+                }
+            od = sum_groups(od);
+            const f4 odr = by_rows(od, vec, g, c);   // O_D of tokens 16tt + 4g + i
+            f4 rcp;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                rcp[i] = __builtin_amdgcn_rcpf(odr[i]);
+            bf8 gh[MP], gl[MP];
+            if constexpr (BFM) {
+#pragma unroll
+                for (int kp = 0; kp < MP; ++kp) {
+                    float g8[8];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        g8[i] = glT[2 * kp][i];
+                        g8[4 + i] = (2 * kp + 1 < MT) ? glT[(2 * kp + 1) % MT][i] : 0.f;
+                    }
+                    split_bf16(g8, gh[kp], gl[kp]);
+                }
+            }
+#pragma unroll
+            for (int ct = 0; ct < 2; ++ct) {
+                f4 on = {0.f, 0.f, 0.f, 0.f};
+                if constexpr (BFM) {
+#pragma unroll
+                    for (int kp = 0; kp < MP; ++kp) {
+                        on = mfma_bf16(gh[kp], wh[kp][ct], on);
+                        on = mfma_bf16(gh[kp], wl[kp][ct], on);
+                        on = mfma_bf16(gl[kp], wh[kp][ct], on);
+                    }
+                } else {
+#pragma unroll
+                    for (int kk = 0; kk < MT; ++kk)
+                        on = mm16_acc(glT[kk], WR[kk][ct], on);
+                }
+                const int f = 16 * ct + c;
+                if (f < d) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        E::store(ou, int64_t(q0 + 16 * tt + 4 * g + i) * d + f, on[i] * rcp[i]);
+                }
+            }
+        }
+    }
+}
+
+// ---- host side ----------------------------------------------------------------
+
+struct Plan {
+    int pieces, piece_len, nchunk, chunk_len, nqchunk, qchunk_len;
+    size_t part, bar, rec, comb, wout, bytes;   // byte offsets of the regions, total
+};
+
+constexpr int64_t kTargetBlocks = 2048;   // workgroups per streaming pass (8 per CU)
+
+int64_t ceil_div(int64_t x, int64_t y) { return (x + y - 1) / y; }
+int64_t round_up(int64_t x, int64_t y) { return ceil_div(x, y) * y; }
+
+// Chunk length for a streaming pass: enough chunks for kTargetBlocks
+// workgroups over all units, at least `lo` and at most `hi` tokens, a
+// multiple of `mult`.
+int chunk_length(int64_t units, int N, int mult, int lo, int hi)
+{
+    const int64_t per_unit = ceil_div(kTargetBlocks, units);
+    int64_t len = round_up(ceil_div(N, per_unit), mult);
+    len = len < lo ? lo : (len > hi ? hi : len);
+    const int64_t whole = round_up(N, mult);
+    return int(len < whole ? len : whole);
+}
+
+Plan make_plan(const Problem &p)
+{
+    Plan s;
+    const int P = p.geo.pr * p.geo.pc;
+    const int64_t units = p.units > 0 ? p.units : 1;
+    int pieces = int(ceil_div(kTargetBlocks, units * p.m));
+    const int most = P / 64 > 1 ? P / 64 : 1;   // pieces of at least 64 tokens
+    pieces = pieces < 1 ? 1 : (pieces > most ? most : pieces);
+    s.piece_len = int(ceil_div(P, pieces));
+    s.pieces = int(ceil_div(P, s.piece_len));
+    s.chunk_len = chunk_length(units, p.N, 32, 256, 4096);
+    s.nchunk = int(ceil_div(p.N, s.chunk_len));
+    s.qchunk_len = chunk_length(units, p.N, 16 * kWaves * 2, 256, 4096);
+    s.nqchunk = int(ceil_div(p.N, s.qchunk_len));
+    size_t off = 0;
+    auto region = [&](size_t floats) {
+        const size_t at = off;
+        off += round_up(int64_t(floats * sizeof(float)), 256);
+        return at;
+    };
+    const size_t u = size_t(units);
+    s.part = region(u * 2 * size_t(p.m) * s.pieces * kWP);
+    s.bar = region(u * 2 * kLm * kWP);
+    s.rec = region(u * size_t(s.nchunk) * kRec);
+    s.comb = region(u * kRec);
+    s.wout = region(u * kWout);
+    s.bytes = off;
+    return s;
+}
+
+template <class E, int MT, int D>
+void launch_split_md(const Problem &p, const Plan &s, const SplitArgs &a, hipStream_t stream)
+{
+    const auto *q = static_cast<const typename E::T *>(p.q);
+    const auto *k = static_cast<const typename E::T *>(p.k);
+    const auto *v = static_cast<const typename E::T *>(p.v);
+    auto *o = static_cast<typename E::T *>(p.o);
+    const unsigned U = unsigned(p.units);
+    const dim3 block(64 * kWaves);
+    hipLaunchKernelGGL((split_pool_kernel<E, D>), dim3(U * unsigned(p.m * s.pieces)), block, 0,
+                       stream, q, k, a);
+    hipLaunchKernelGGL(split_bar_kernel, dim3(U), dim3(256), 0, stream, a);
+    const bool bfm = E::bytes == 2 && p.N % 32 == 0;
+    if (bfm)
+        hipLaunchKernelGGL((split_keys_kernel<E, MT, D, E::bytes == 2>),
+                           dim3(U * unsigned(s.nchunk)), block, 0, stream, k, v, a);
+    else
+        hipLaunchKernelGGL((split_keys_kernel<E, MT, D, false>), dim3(U * unsigned(s.nchunk)),
+                           block, 0, stream, k, v, a);
+    hipLaunchKernelGGL(split_merge_kernel, dim3(U * unsigned(MT * kMergeGroups)), dim3(256), 0,
+                       stream, a, MT);
+    const size_t lds = size_t(LargeLds<MT>::total) * sizeof(float);
+    if (bfm)
+        hipLaunchKernelGGL((split_core_kernel<MT, D, E::bytes == 2>), dim3(U), dim3(64 * MT), lds,
+                           stream, a);
+    else
+        hipLaunchKernelGGL((split_core_kernel<MT, D, false>), dim3(U), dim3(64 * MT), lds, stream,
+                           a);
+    if (bfm)
+        hipLaunchKernelGGL((split_query_kernel<E, MT, D, E::bytes == 2>),
+                           dim3(U * unsigned(s.nqchunk)), block, 0, stream, q, o, a);
+    else
+        hipLaunchKernelGGL((split_query_kernel<E, MT, D, false>), dim3(U * unsigned(s.nqchunk)),
+                           block, 0, stream, q, o, a);
+}
+
+template <class E, int D>
+void launch_split_d(const Problem &p, const Plan &s, const SplitArgs &a, hipStream_t stream)
+{
+    switch ((p.m + 15) / 16) {
+    case 1: launch_split_md<E, 1, D>(p, s, a, stream); break;
+    case 2: launch_split_md<E, 2, D>(p, s, a, stream); break;
+    case 3: launch_split_md<E, 3, D>(p, s, a, stream); break;
+    default: launch_split_md<E, 4, D>(p, s, a, stream); break;
+    }
+}
+
+template <class E>
+void launch_split_e(const Problem &p, const Plan &s, const SplitArgs &a, hipStream_t stream)
+{
+    switch (p.d) {
+    case 8: launch_split_d<E, 8>(p, s, a, stream); break;
+    case 16: launch_split_d<E, 16>(p, s, a, stream); break;
+    case 24: launch_split_d<E, 24>(p, s, a, stream); break;
+    case 30: launch_split_d<E, 30>(p, s, a, stream); break;
+    default: launch_split_d<E, 32>(p, s, a, stream); break;
+    }
+}
+
+}  // namespace
+
+bool split_supported(const Problem &p)
+{
+    if (p.N % 16 != 0 || p.m > 64 || !tiled_width(p.d))
+        return false;
+    if (p.dtype == 1) {   // 16-byte row pieces of bf16 need 4-byte aligned rows
+        const uintptr_t mis = uintptr_t(p.q) | uintptr_t(p.k) | uintptr_t(p.v);
+        if (mis % 4 != 0)
+            return false;
+    }
+    // every grid within the 2^32 work-items of one dispatch dimension
+    const Plan s = make_plan(p);
+    int64_t most = s.nchunk > s.nqchunk ? s.nchunk : s.nqchunk;
+    if (int64_t(p.m) * s.pieces > most)
+        most = int64_t(p.m) * s.pieces;
+    if (most < 4 * kMergeGroups)
+        most = 4 * kMergeGroups;
+    return p.units * most * 256 < (int64_t(1) << 32);
+}
+
+size_t split_workspace_bytes(const Problem &p) { return make_plan(p).bytes; }
+
+hipError_t launch_split(const Problem &p, void *workspace, hipStream_t stream)
+{
+    const Plan s = make_plan(p);
+    char *ws = static_cast<char *>(workspace);
+    SplitArgs a;
+    a.units = p.units;
+    a.N = p.N;
+    a.d = p.d;
+    a.m = p.m;
+    a.iters = p.iters;
+    a.s2 = p.scale * kLog2e;
+    a.P = p.geo.pr * p.geo.pc;
+    a.inv_patch = 1.0f / float(a.P);
+    a.cols = p.geo.cols;
+    a.pr = p.geo.pr;
+    a.pc = p.geo.pc;
+    a.gc = p.geo.gc;
+    a.pieces = s.pieces;
+    a.piece_len = s.piece_len;
+    a.nchunk = s.nchunk;
+    a.chunk_len = s.chunk_len;
+    a.nqchunk = s.nqchunk;
+    a.qchunk_len = s.qchunk_len;
+    a.part = reinterpret_cast<float *>(ws + s.part);
+    a.bar = reinterpret_cast<float *>(ws + s.bar);
+    a.rec = reinterpret_cast<float *>(ws + s.rec);
+    a.comb = reinterpret_cast<float *>(ws + s.comb);
+    a.wout = reinterpret_cast<float *>(ws + s.wout);
+    if (p.dtype == 0)
+        launch_split_e<F32>(p, s, a, stream);
+    else
+        launch_split_e<BF16>(p, s, a, stream);
+    return hipGetLastError();
+}
+
+}  // namespace nystra

@@ -15,7 +15,7 @@ from paper_2506_08520_amd import binding as B
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "nystra.h")
 
-OK, ENULL, ESHAPE, EDTYPE, EALIGN, EOVERLAP, EUNSUP, EHIP, EARG = range(9)
+OK, ENULL, ESHAPE, EDTYPE, EALIGN, EOVERLAP, EUNSUP, EHIP, EARG, EWS = range(10)
 
 
 def declared_functions():
@@ -93,9 +93,11 @@ def test_forward_validation(L):
     seg = B.make_opts(landmark_mode=1)
     assert fwd(L, N=64, m=5, opts=seg) == ESHAPE
     for o in [B.make_opts(pinv_iters=-1), B.make_opts(pinv_iters=65), B.make_opts(landmark_mode=2),
-              B.make_opts(variant=3), B.make_opts(scale=float("nan")),
+              B.make_opts(variant=4), B.make_opts(variant=-1), B.make_opts(scale=float("nan")),
               B.make_opts(scale=float("inf"))]:
         assert fwd(L, opts=o) == EARG
+    # the token-split kernels need a workspace, which this entry point lacks
+    assert fwd(L, opts=B.make_opts(variant=B.VARIANT_SPLIT)) == EUNSUP
     assert fwd(L, q=None) == ENULL
     assert fwd(L, o=None) == ENULL
     assert fwd(L, q=P + 2) == EALIGN
@@ -146,7 +148,7 @@ def test_landmark_pool_validation(L):
 
 
 def test_status_strings_and_opts(L):
-    for s in range(9):
+    for s in range(10):
         assert B.nystra_status_str(s) and B.nystra_status_str(s) != "unknown status"
     assert B.nystra_status_str(99) == "unknown status"
     o = B.nystra_default_opts()
@@ -164,3 +166,63 @@ def test_variant_selection():
     with pytest.raises(B.NystraError):
         B.nystra_select_variant(64, 30, 16, opts=B.make_opts(pinv_iters=-3))
 
+
+
+def ws_size(W, H, N, d, m, dtype=0, **opts):
+    return B.nystra_attn_workspace_size(W, H, N, d, m, dtype, B.make_opts(**opts))
+
+
+def test_workspace_size():
+    split = B.VARIANT_SPLIT
+    # global window, few units: AUTO takes the token-split kernels
+    big = ws_size(1, 6, 1 << 18, 32, 64)
+    assert 0 < big < 64 << 20
+    assert ws_size(1, 6, 1 << 18, 32, 64, 1) == big   # fp32 records for either dtype
+    # one workgroup per unit fills the GPU: no workspace
+    assert ws_size(1024, 6, 64, 30, 16) == 0
+    assert ws_size(256, 8, 1024, 32, 64) == 0
+    # forced: any supported shape, sized from the same plan
+    assert ws_size(1024, 6, 64, 30, 16, variant=split) > 0
+    assert ws_size(1, 6, 1 << 18, 32, 64, variant=split) == big
+    assert ws_size(1, 6, 1 << 18, 32, 64, variant=B.VARIANT_TILED) == 0
+    assert ws_size(1, 6, 1 << 18, 32, 64, variant=B.VARIANT_GENERIC) == 0
+    # more tokens, more chunk records
+    assert ws_size(1, 2, 1 << 16, 32, 64) < ws_size(1, 2, 1 << 18, 32, 64)
+    assert ws_size(0, 6, 1 << 18, 32, 64) == 0
+    # shapes the token-split kernels do not cover
+    for args in [(1, 1, 16384, 20, 64), (1, 1, 100, 32, 4), (1, 1, 16384, 48, 64)]:
+        with pytest.raises(B.NystraError) as e:
+            ws_size(*args, variant=split)
+        assert e.value.status == EUNSUP
+        assert ws_size(*args) == 0   # AUTO falls back to the other kernels
+    with pytest.raises(B.NystraError) as e:
+        ws_size(1, 1, 63, 32, 7)
+    assert e.value.status == ESHAPE
+    assert B.lib().nystra_attn_workspace_size(1, 1, 4096, 32, 16, 0, None, None) == ENULL
+
+
+def test_forward_ws_validation(L):
+    q, k, v, o = P, P + (1 << 24), P + (2 << 24), P + (3 << 24)
+    ws = P + (4 << 24)
+    N, d, m = 4096, 32, 16
+    need = ws_size(1, 2, N, d, m)
+    assert need > 0
+    opts = B.make_opts()
+
+    def f(ws=ws, nbytes=need, q=q, o=o, N=N, opts=opts):
+        return L.nystra_attn_forward_ws(q, k, v, o, 1, 2, N, d, m, 0, ctypes.byref(opts), ws,
+                                        nbytes, None)
+
+    # every failure below is detected before anything is enqueued
+    assert f(ws=None) == EWS
+    assert f(nbytes=need - 1) == EWS
+    assert f(ws=ws + 128) == EWS          # not 256-byte aligned
+    assert f(ws=q + 256) == EWS           # overlaps Q
+    assert f(ws=o - 1024) == EWS          # runs into O
+    assert f(q=None) == ENULL
+    assert f(o=q + 64) == EOVERLAP
+    assert f(N=4095) == ESHAPE
+    assert f(opts=B.make_opts(variant=5)) == EARG
+    assert f(opts=B.make_opts(variant=B.VARIANT_SPLIT), N=4096 + 16) == ESHAPE  # no 2-D grid
+    assert L.nystra_attn_forward_ws(None, None, None, None, 0, 2, N, d, m, 0, None, None, 0,
+                                    None) == OK

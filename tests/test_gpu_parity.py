@@ -33,6 +33,15 @@ def run(q, k, v, m, dtype, variant, iters=6, mode=0, scale=0.0):
     return out
 
 
+def run_ws(q, k, v, m, dtype, variant, iters=6, mode=0, scale=0.0, workspace=None):
+    """The workspace entry point (torch allocates the workspace it asks for)."""
+    tq, tk, tv = (to_dev(x, dtype) for x in (q, k, v))
+    opts = B.make_opts(pinv_iters=iters, landmark_mode=mode, scale=scale, variant=variant)
+    o = B.nystra_attn_forward_ws(tq, tk, tv, m, opts=opts, workspace=workspace)
+    torch.cuda.synchronize()
+    return to_host(o)
+
+
 def check_config(got, ref, dtype, what):
     """Parity bar for the configuration workloads.
 
@@ -267,15 +276,82 @@ GLOBAL = [(2, 16384, 32, 64, 0, "f32"), (2, 16384, 32, 16, 1, "f32"), (1, 16384,
           (2, 65536, 32, 64, 0, "f32"), (2, 65536, 32, 64, 0, "bf16"), (2, 16384, 30, 32, 0, "bf16")]
 
 
+@pytest.mark.parametrize("entry", ["ex", "ws"])
 @pytest.mark.parametrize("shape", GLOBAL, ids=lambda s: "x".join(map(str, s)))
-def test_global_window(shape):
+def test_global_window(shape, entry):
+    """Both entry points with AUTO: the one-pass kernels through _ex, the
+    token-split kernels (where they cover the shape) through _ws."""
     h, N, d, m, mode, dtype = shape
     q, k, v = W.iid((1, h, N, d), seed=N + d + m + mode, dtype=dtype)
     ref = oracle.forward(q, k, v, m, iters=6, mode=mode)
-    got = run(q, k, v, m, dtype, B.VARIANT_AUTO, mode=mode)
+    if entry == "ex":
+        got = run(q, k, v, m, dtype, B.VARIANT_AUTO, mode=mode)
+    else:
+        code = B.F32 if dtype == "f32" else B.BF16
+        ws = B.nystra_attn_workspace_size(1, h, N, d, m, code, B.make_opts(landmark_mode=mode))
+        assert (ws > 0) == (d in (8, 16, 24, 30, 32))
+        got = run_ws(q, k, v, m, dtype, B.VARIANT_AUTO, mode=mode)
     err = error(got, ref, dtype)
-    print(f"N={N} d={d} m={m} mode={mode} {dtype}: error {err:.3e}")
+    print(f"N={N} d={d} m={m} mode={mode} {dtype} {entry}: error {err:.3e}")
     assert err <= TOL[dtype]
+
+
+# The token-split kernels forced through the workspace entry point:
+# (n_windows, heads, N, d, m, mode, dtype).  N = 10000 has 25 x 25 patches
+# (pieces and tiles straddle patch rows) and N % 32 == 16 (bf16 then takes the
+# fp32 matrix-core path, and the last key chunk ends on an unpaired tile).
+SPLIT = [(1, 2, 1024, 32, 16, 0, "f32"), (2, 3, 256, 30, 32, 0, "bf16"),
+         (1, 1, 4096, 8, 64, 1, "f32"), (1, 2, 10000, 32, 16, 0, "f32"),
+         (1, 2, 10000, 24, 16, 0, "bf16"), (1, 1, 2304, 16, 9, 0, "f32"),
+         (1, 2, 16384, 32, 64, 0, "f32"), (1, 2, 20736, 30, 48, 0, "bf16"),
+         (2, 1, 65536, 32, 64, 0, "bf16"), (1, 1, 65536, 16, 8, 1, "f32"),
+         (16, 6, 64, 30, 16, 0, "f32"), (4, 8, 1024, 32, 64, 0, "bf16")]
+
+
+@pytest.mark.parametrize("shape", SPLIT, ids=lambda s: "x".join(map(str, s)))
+def test_split_kernels(shape):
+    nw, h, N, d, m, mode, dtype = shape
+    q, k, v = W.iid((nw, h, N, d), seed=3 * N + d + m, dtype=dtype)
+    ref = oracle.forward(q, k, v, m, iters=6, mode=mode)
+    got = run_ws(q, k, v, m, dtype, B.VARIANT_SPLIT, mode=mode)
+    err = error(got, ref, dtype)
+    print(f"{shape}: error {err:.3e}")
+    assert err <= TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("order", ["rising", "falling"])
+def test_split_running_max_order(order, dtype):
+    """The chunk maxima rise (or fall) from chunk to chunk, so the merge
+    rescales every chunk record but the last (or first)."""
+    nw, h, N, d, m = 1, 2, 4096, 32, 16
+    q, k, v = W.iid((nw, h, N, d), seed=11 + len(order), dtype=dtype)
+    u = np.abs(q).mean(axis=2, keepdims=True)
+    ramp = np.linspace(-1.0, 1.0, N)[None, None, :, None]
+    if order == "falling":
+        ramp = ramp[:, :, ::-1]
+    k = W.round_to(k + 3.0 * ramp * np.sign(q.mean(axis=2, keepdims=True)) * (u > 0), dtype)
+    ref = oracle.forward(q, k, v, m, iters=6, mode=0)
+    got = run_ws(q, k, v, m, dtype, B.VARIANT_SPLIT)
+    assert error(got, ref, dtype, storage_floor=True) <= TOL[dtype]
+
+
+def test_split_deterministic_and_workspace_reuse():
+    """No atomics: repeated calls give identical bits, also when the workspace
+    still holds the records of a different, larger problem."""
+    q, k, v = W.iid((1, 2, 16384, 32), seed=5)
+    tq, tk, tv = (to_dev(x, "f32") for x in (q, k, v))
+    opts = B.make_opts(variant=B.VARIANT_SPLIT)
+    big = B.nystra_attn_workspace_size(1, 4, 65536, 32, 64, B.F32, opts)
+    ws = torch.full((big,), 0xFF, dtype=torch.uint8, device="cuda")   # NaN patterns
+    a = B.nystra_attn_forward_ws(tq, tk, tv, 16, opts=opts, workspace=ws)
+    qq, kk, vv = (to_dev(x, "f32") for x in W.iid((1, 4, 65536, 32), seed=6))
+    B.nystra_attn_forward_ws(qq, kk, vv, 64, opts=opts, workspace=ws)
+    b = B.nystra_attn_forward_ws(tq, tk, tv, 16, opts=opts, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+    ref = oracle.forward(q, k, v, 16, iters=6, mode=0)
+    assert error(to_host(a), ref, "f32") <= TOL["f32"]
 
 
 def test_exact_kernel_long_window():
