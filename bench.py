@@ -200,9 +200,11 @@ def sweep(args):
             tq, tk, tv = (x.to(tdt) for x in (q, k, v))
             ex = torch.empty_like(tq)
             reps = max(3, min(50, int(2e5 // (wl.units * N / 64))))
-            t_ex = timed(lambda: B.nystra_exact_attn_forward(tq, tk, tv, out=ex), reps)
-            exf = ex.float()
-            ref_rms = float(exf.pow(2).mean().sqrt())
+            t_ex = exf = None
+            if not args.no_exact:
+                t_ex = timed(lambda: B.nystra_exact_attn_forward(tq, tk, tv, out=ex), reps)
+                exf = ex.float()
+                ref_rms = float(exf.pow(2).mean().sqrt())
             for m in (int(x) for x in args.sweep_m.split(",")):
                 if m > N:
                     continue
@@ -227,7 +229,7 @@ def sweep(args):
                     wsa = torch.empty(max(na, 1), dtype=torch.uint8, device="cuda")
                     t = timed(lambda: B.nystra_attn_forward_ws(tq, tk, tv, m, opts=opts,
                                                                workspace=wsa, out=o), reps)
-                    diff = (o.float() - exf)
+                    diff = (o.float() - exf) if exf is not None else None
                     one = names[B.nystra_select_variant(N, d, m, code, opts)]
                     print(json.dumps({
                         "N": N, "m": m, "K": K, "dtype": dt, "units": wl.units,
@@ -235,10 +237,12 @@ def sweep(args):
                         "nystra_us": round(t * 1e3, 2), "onepass_variant": one,
                         "onepass_us": round(t1 * 1e3, 2),
                         "split_us": round(t_split * 1e3, 2) if t_split else None,
-                        "exact_us": round(t_ex * 1e3, 2),
-                        "speedup_vs_exact": round(t_ex / t, 3),
-                        "rel_rms_err_vs_exact": float(diff.pow(2).mean().sqrt()) / ref_rms,
-                        "max_abs_err_vs_exact": float(diff.abs().max())}), flush=True)
+                        "exact_us": round(t_ex * 1e3, 2) if t_ex else None,
+                        "speedup_vs_exact": round(t_ex / t, 3) if t_ex else None,
+                        "rel_rms_err_vs_exact":
+                            float(diff.pow(2).mean().sqrt()) / ref_rms if t_ex else None,
+                        "max_abs_err_vs_exact": float(diff.abs().max()) if t_ex else None}),
+                          flush=True)
                     del wsa
         del q, k, v, tq, tk, tv, ex
         torch.cuda.empty_cache()

@@ -131,31 +131,47 @@ split_pool_kernel(const typename E::T *__restrict__ q, const typename E::T *__re
 }
 
 // ---- A2: Qbar and Kbar -----------------------------------------------------
-__global__ void __launch_bounds__(256) split_bar_kernel(SplitArgs a)
+// One wave per row (unit, tensor, landmark < kLm): the two halves of the wave
+// add alternate pieces, then each other's sums.  Rows past m are zero.
+__global__ void __launch_bounds__(64) split_bar_kernel(SplitArgs a)
 {
-    const int64_t unit = blockIdx.x;
-    const int per_unit = a.m * a.pieces;
-    for (int idx = threadIdx.x; idx < 2 * kLm * kWP; idx += blockDim.x) {
-        const int which = idx / (kLm * kWP), l = (idx / kWP) % kLm, f = idx % kWP;
-        float acc = 0.f;
-        if (l < a.m && f < a.d) {
-            const float *p = a.part + ((unit * 2 + which) * per_unit + l * a.pieces) * kWP + f;
-            for (int r = 0; r < a.pieces; ++r)
-                acc += p[int64_t(r) * kWP];
-            acc *= a.inv_patch;
+    const int64_t row = blockIdx.x;   // (unit * 2 + which) * kLm + l
+    const int l = int(row % kLm);
+    const int64_t uw = row / kLm;     // unit * 2 + which
+    const int half = threadIdx.x >> 5, f = threadIdx.x & 31;
+    float acc = 0.f;
+    if (l < a.m && f < a.d) {
+        const float *p = a.part + (uw * a.m + l) * int64_t(a.pieces) * kWP + f;
+        float acc2 = 0.f;
+        int r = half;
+        for (; r + 2 < a.pieces; r += 4) {
+            acc += p[int64_t(r) * kWP];
+            acc2 += p[int64_t(r + 2) * kWP];
         }
-        a.bar[unit * 2 * kLm * kWP + idx] = acc;
+        if (r < a.pieces)
+            acc += p[int64_t(r) * kWP];
+        acc += acc2;
     }
+    acc += __shfl_xor(acc, 32, 64);
+    if (half == 0)
+        a.bar[row * kWP + f] = (l < a.m && f < a.d) ? acc * a.inv_patch : 0.f;
 }
 
 // ---- B: chunk records of the G_U side ----------------------------------------
+// With d_h % 16 != 0 the first padding column of V is set to 1, so T_D
+// accumulates on the matrix cores as column d_h of T; NCT feature tiles of
+// 16 columns cover the features (and that column).
 template <class E, int MT, int D, bool BFM>
 __global__ void __launch_bounds__(64 * kWaves)
 split_keys_kernel(const typename E::T *__restrict__ k, const typename E::T *__restrict__ v,
                   SplitArgs a)
 {
     constexpr int d = D;
-    __shared__ float recs[kWaves][kRec];
+    constexpr bool kOnes = D % 16 != 0;
+    constexpr int NCT = (D + 15) / 16;
+    // per-wave records in LDS: T rows of the MT tiles, then T_D, then maxima
+    constexpr int RR = 16 * MT, LD = RR * kWP, LM = LD + RR, LREC = LD + 2 * RR;
+    __shared__ __align__(16) float recs[kWaves][LREC];
     __shared__ float vecs[kWaves][64];
     const int64_t unit = blockIdx.x / a.nchunk;
     const int chunk = int(blockIdx.x - unit * a.nchunk);
@@ -181,11 +197,13 @@ split_keys_kernel(const typename E::T *__restrict__ k, const typename E::T *__re
             split_bf16(qb[j], qbh[j], qbl[j]);
     }
 
-    f4 T[MT][2];
+    f4 T[MT][NCT];
     float tden[MT], mrun[MT];
 #pragma unroll
     for (int j = 0; j < MT; ++j) {
-        T[j][0] = T[j][1] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct)
+            T[j][ct] = f4{0.f, 0.f, 0.f, 0.f};
         tden[j] = 0.f;
         mrun[j] = -INFINITY;
     }
@@ -195,9 +213,9 @@ split_keys_kernel(const typename E::T *__restrict__ k, const typename E::T *__re
     // the chunk's end (fp32 path with an odd tile count) repeats the first and
     // is not accumulated.
     for (int t0 = 2 * w; t0 < NT; t0 += 2 * kWaves) {
-        float kr[2][8], vr[2][2][4];
+        float kr[2][8], vr[2][NCT][4];
         bf8 kw[2];
-        uint16_t vh[2][2][4];
+        uint16_t vh[2][NCT][4];
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
             const int tt = min(t0 + u, NT - 1);
@@ -207,25 +225,36 @@ split_keys_kernel(const typename E::T *__restrict__ k, const typename E::T *__re
             else
                 load_chunk8<E, D>(ku + row, g, kr[u]);
 #pragma unroll
-            for (int ct = 0; ct < 2; ++ct) {
+            for (int ct = 0; ct < NCT; ++ct) {
                 const int f = 16 * ct + c;
 #pragma unroll
                 for (int s = 0; s < 4; ++s) {
                     const int64_t idx = int64_t(k0 + 16 * tt + 4 * g + s) * d + min(f, d - 1);
                     if constexpr (BFM) {
                         const uint16_t x = vu16[idx];
-                        vh[u][ct][s] = f < d ? x : uint16_t(0);
+                        vh[u][ct][s] = f < d ? x : uint16_t(kOnes && f == d ? 0x3F80u : 0u);
                     } else {
                         const float x = E::load(vu, idx);
-                        vr[u][ct][s] = f < d ? x : 0.f;
+                        vr[u][ct][s] = f < d ? x : (kOnes && f == d ? 1.f : 0.f);
                     }
                 }
             }
         }
         const bool second = t0 + 1 < NT;   // uniform
+        bf8 vv[NCT];   // bf16 path: V of the pair as the right-hand operand
+        if constexpr (BFM) {
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) {
+                U16B vb;
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj)
+                    vb.w[jj] = uint32_t(vh[jj >> 1][ct][2 * (jj & 1)]) |
+                               (uint32_t(vh[jj >> 1][ct][2 * (jj & 1) + 1]) << 16);
+                vv[ct] = __builtin_bit_cast(bf8, vb);
+            }
+        }
 #pragma unroll
         for (int j = 0; j < MT; ++j) {
-            const bool lval = 16 * j + c < m;
             // S_U^T tiles: lane (g, c) gets S_U[landmark 16j + c][key 16tt + 4g + i].
             f4 su[2];
             float gmax = -INFINITY;
@@ -251,32 +280,29 @@ split_keys_kernel(const typename E::T *__restrict__ k, const typename E::T *__re
                 const float f = fast_exp2(a.s2 * (mrun[j] - mnew));
                 tden[j] *= f;
                 const f4 fr = by_rows(f, vec, g, c);   // factor of landmark 16j + 4g + i
-                T[j][0] *= fr;
-                T[j][1] *= fr;
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct)
+                    T[j][ct] *= fr;
             }
             mrun[j] = mnew;
-            const float mb = a.s2 * mnew;
+            // Landmarks past m get an infinite offset: their terms are exactly 0.
+            const float mb = 16 * j + c < m ? a.s2 * mnew : INFINITY;
             if constexpr (BFM) {
                 float gk[8];
 #pragma unroll
                 for (int h = 0; h < 2; ++h)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        gk[4 * h + i] = lval ? fast_exp2(fmaf(a.s2, su[h][i], -mb)) : 0.f;
-                        tden[j] += gk[4 * h + i];
+                        gk[4 * h + i] = fast_exp2(fmaf(a.s2, su[h][i], -mb));
+                        if constexpr (!kOnes)
+                            tden[j] += gk[4 * h + i];
                     }
                 bf8 gh, gl;
                 split_bf16(gk, gh, gl);
 #pragma unroll
-                for (int ct = 0; ct < 2; ++ct) {
-                    U16B vb;
-#pragma unroll
-                    for (int jj = 0; jj < 4; ++jj)
-                        vb.w[jj] = uint32_t(vh[jj >> 1][ct][2 * (jj & 1)]) |
-                                   (uint32_t(vh[jj >> 1][ct][2 * (jj & 1) + 1]) << 16);
-                    const bf8 vv = __builtin_bit_cast(bf8, vb);
-                    T[j][ct] = mfma_bf16(gh, vv, T[j][ct]);
-                    T[j][ct] = mfma_bf16(gl, vv, T[j][ct]);
+                for (int ct = 0; ct < NCT; ++ct) {
+                    T[j][ct] = mfma_bf16(gh, vv[ct], T[j][ct]);
+                    T[j][ct] = mfma_bf16(gl, vv[ct], T[j][ct]);
                 }
             } else {
 #pragma unroll
@@ -286,11 +312,12 @@ split_keys_kernel(const typename E::T *__restrict__ k, const typename E::T *__re
                     f4 e;
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        e[i] = lval ? fast_exp2(fmaf(a.s2, su[u][i], -mb)) : 0.f;
-                        tden[j] += e[i];
+                        e[i] = fast_exp2(fmaf(a.s2, su[u][i], -mb));
+                        if constexpr (!kOnes)
+                            tden[j] += e[i];
                     }
 #pragma unroll
-                    for (int ct = 0; ct < 2; ++ct)
+                    for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
                         for (int s = 0; s < 4; ++s)
                             T[j][ct] = mfma4(e[s], vr[u][ct][s], T[j][ct]);
@@ -303,15 +330,19 @@ split_keys_kernel(const typename E::T *__restrict__ k, const typename E::T *__re
     float *rw = recs[w];
 #pragma unroll
     for (int j = 0; j < MT; ++j) {
-        const float td = sum_groups(tden[j]);
 #pragma unroll
         for (int ct = 0; ct < 2; ++ct)
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                rw[(16 * j + 4 * g + i) * kWP + 16 * ct + c] = T[j][ct][i];
+            for (int i = 0; i < 4; ++i) {
+                float x = 0.f;
+                if (ct < NCT)
+                    x = T[j][ct < NCT ? ct : 0][i];
+                rw[(16 * j + 4 * g + i) * kWP + 16 * ct + c] = x;
+            }
+        const float td = kOnes ? 0.f : sum_groups(tden[j]);
         if (g == 0) {
-            rw[kRecD + 16 * j + c] = td;
-            rw[kRecM + 16 * j + c] = mrun[j];
+            rw[LD + 16 * j + c] = td;
+            rw[LM + 16 * j + c] = mrun[j];
         }
     }
     __syncthreads();
@@ -321,14 +352,14 @@ split_keys_kernel(const typename E::T *__restrict__ k, const typename E::T *__re
         float mx = -INFINITY;
 #pragma unroll
         for (int v = 0; v < kWaves; ++v)
-            mx = fmaxf(mx, recs[v][kRecM + l]);
+            mx = fmaxf(mx, recs[v][LM + l]);
         f4 acc = {0.f, 0.f, 0.f, 0.f};
         float den = 0.f;
 #pragma unroll
         for (int v = 0; v < kWaves; ++v) {
-            const float fw = fast_exp2(a.s2 * (recs[v][kRecM + l] - mx));   // 0 for an idle wave
+            const float fw = fast_exp2(a.s2 * (recs[v][LM + l] - mx));   // 0 for an idle wave
             acc += fw * *reinterpret_cast<const f4 *>(&recs[v][l * kWP + f]);
-            den += fw * recs[v][kRecD + l];
+            den += fw * recs[v][kOnes ? l * kWP + d : LD + l];
         }
         *reinterpret_cast<f4 *>(out + l * kWP + f) = acc;
         if (f == 0) {
@@ -341,12 +372,13 @@ split_keys_kernel(const typename E::T *__restrict__ k, const typename E::T *__re
 // ---- C: merge of the chunk records ------------------------------------------
 // Block (unit, landmark tile j, column group q): q < 8 merges features
 // 4q .. 4q+3 of T, q = 8 the column T_D.  Four slices of 64 threads take every
-// fourth chunk; thread (landmark li, column x) of a slice keeps its maximum and
-// sum, and the slices are merged in LDS in a fixed order.  Every block of a
-// tile computes the same maxima (a max is exact), and block q = 0 stores
-// s2 * m_U.
+// fourth chunk; thread (landmark li, column x) of a slice keeps a running
+// maximum and the sum against it, eight chunk records in flight per step, and
+// the slices are merged in LDS in a fixed order.  Every block of a tile
+// computes the same maxima (a max is exact); block q = 0 stores s2 * m_U.
 __global__ void __launch_bounds__(256) split_merge_kernel(SplitArgs a, int MT)
 {
+    constexpr int kU = 8;
     __shared__ float smax[4][64], ssum[4][64];
     const int per_unit = MT * kMergeGroups;
     const int64_t unit = blockIdx.x / per_unit;
@@ -357,13 +389,31 @@ __global__ void __launch_bounds__(256) split_merge_kernel(SplitArgs a, int MT)
     const int l = 16 * j + li;
     const int col = q < kMergeGroups - 1 ? l * kWP + 4 * q + x : kRecD + l;
     const float *rec = a.rec + unit * a.nchunk * kRec;
-    float mx = -INFINITY;
-    for (int ch = slice; ch < a.nchunk; ch += 4)
-        mx = fmaxf(mx, rec[int64_t(ch) * kRec + kRecM + l]);
-    float sum = 0.f;
-    for (int ch = slice; ch < a.nchunk; ch += 4) {
+    float mx = -INFINITY, sum = 0.f;
+    int ch = slice;
+    for (; ch + 4 * (kU - 1) < a.nchunk; ch += 4 * kU) {
+        float cm[kU], cv[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const float *r = rec + int64_t(ch + 4 * u) * kRec;
+            cm[u] = r[kRecM + l];
+            cv[u] = r[col];
+        }
+        float nm = mx;
+#pragma unroll
+        for (int u = 0; u < kU; ++u)
+            nm = fmaxf(nm, cm[u]);
+        sum *= fast_exp2(a.s2 * (mx - nm));   // 0 * 0 on the first step
+#pragma unroll
+        for (int u = 0; u < kU; ++u)
+            sum = fmaf(fast_exp2(a.s2 * (cm[u] - nm)), cv[u], sum);
+        mx = nm;
+    }
+    for (; ch < a.nchunk; ch += 4) {
         const float *r = rec + int64_t(ch) * kRec;
-        sum += fast_exp2(a.s2 * (r[kRecM + l] - mx)) * r[col];
+        const float cm = r[kRecM + l], nm = fmaxf(mx, cm);
+        sum = fmaf(fast_exp2(a.s2 * (cm - nm)), r[col], sum * fast_exp2(a.s2 * (mx - nm)));
+        mx = nm;
     }
     smax[slice][t] = mx;
     ssum[slice][t] = sum;
@@ -416,39 +466,57 @@ __global__ void __launch_bounds__(64 * MT) split_core_kernel(SplitArgs a)
 }
 
 // ---- D: Steps 3 (G_L side), 6 and 7 -----------------------------------------
+// With d_h % 16 != 0, column d_h of W holds Z T_D (the ones column of pass B),
+// so O_D is column d_h of G_L^n W and comes out of the same products.  Each
+// tile of O goes through a per-wave LDS stage and leaves as contiguous 16-byte
+// pieces (O 16-byte aligned).  Landmark masks are compiled out when m fills
+// its tiles.
+template <bool B>
+struct Flag {
+    static constexpr bool value = B;
+};
+
 template <class E, int MT, int D, bool BFM>
 __global__ void __launch_bounds__(64 * kWaves)
 split_query_kernel(const typename E::T *__restrict__ q, typename E::T *__restrict__ o,
                    SplitArgs a)
 {
     constexpr int d = D;
+    constexpr bool kOnes = D % 16 != 0;
+    constexpr int NCT = (D + 15) / 16;
     constexpr int TDo = table_den<MT>();
     constexpr int MP = (MT + 1) / 2;   // landmark tile pairs (bf16 path)
+    constexpr int kStageBytes = 16 * D * E::bytes;   // one 16-token tile of O
+    constexpr int kPieces = kStageBytes / 16;
+    __shared__ __align__(16) char stages[kWaves][kStageBytes];
     __shared__ float vecs[kWaves][64];
     const int64_t unit = blockIdx.x / a.nqchunk;
     const int qc = int(blockIdx.x - unit * a.nqchunk);
     const int w = wave_id(), lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
     float *vec = vecs[w];
+    char *stage = stages[w];
     const int m = a.m;
     const int64_t base = unit * int64_t(a.N) * d;
     const typename E::T *qu = q + base;
-    typename E::T *ou = o + base;
+    char *ob = reinterpret_cast<char *>(o + base);
     const float *Wb = a.wout + unit * kWout;
     const float *kbar = a.bar + unit * 2 * kLm * kWP + kLm * kWP;
 
-    f4 WR[MT][2], wdv[MT];
+    f4 WR[MT][NCT], wdv[MT];
     float kb[MT][8];
 #pragma unroll
     for (int kk = 0; kk < MT; ++kk) {
-        WR[kk][0] = read_r<kTS>(Wb, kk, 0, g, c);
-        WR[kk][1] = read_r<kTS>(Wb, kk, 1, g, c);
-        wdv[kk] = *reinterpret_cast<const f4 *>(Wb + TDo + 16 * kk + 4 * g);
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct)
+            WR[kk][ct] = read_r<kTS>(Wb, kk, ct, g, c);
+        if constexpr (!kOnes)
+            wdv[kk] = *reinterpret_cast<const f4 *>(Wb + TDo + 16 * kk + 4 * g);
 #pragma unroll
         for (int s = 0; s < 8; ++s)
             kb[kk][s] = slot_valid<D>(g, s) ? kbar[(16 * kk + c) * kWP + chunk_start<D>(g) + s]
                                             : 0.f;
     }
-    bf8 kbh[MT], kbl[MT], wh[MP][2], wl[MP][2];
+    bf8 kbh[MT], kbl[MT], wh[MP][NCT], wl[MP][NCT];
     if constexpr (BFM) {
 #pragma unroll
         for (int kk = 0; kk < MT; ++kk)
@@ -456,7 +524,7 @@ split_query_kernel(const typename E::T *__restrict__ q, typename E::T *__restric
 #pragma unroll
         for (int kp = 0; kp < MP; ++kp)
 #pragma unroll
-            for (int ct = 0; ct < 2; ++ct) {
+            for (int ct = 0; ct < NCT; ++ct) {
                 float w8[8];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
@@ -470,95 +538,131 @@ split_query_kernel(const typename E::T *__restrict__ q, typename E::T *__restric
     const int q0 = qc * a.qchunk_len, q1 = min(a.N, q0 + a.qchunk_len);
     const int NT = (q1 - q0) >> 4;
     constexpr int kQGroup = 2;
-    for (int t0 = w; t0 < NT; t0 += kQGroup * kWaves) {
-        float qg[kQGroup][8];
-        bf8 qw[kQGroup];
+
+    auto tiles = [&](auto full) {
+        constexpr bool FULL = decltype(full)::value;   // m == 16 MT: no landmark masks
+        for (int t0 = w; t0 < NT; t0 += kQGroup * kWaves) {
+            float qg[kQGroup][8];
+            bf8 qw[kQGroup];
 #pragma unroll
-        for (int u = 0; u < kQGroup; ++u) {
-            const int64_t row = int64_t(q0 + 16 * min(t0 + u * kWaves, NT - 1) + c) * d;
-            if constexpr (BFM)
-                qw[u] = load_chunk8_bf8<D>(qu16 + row, g);
-            else
-                load_chunk8<E, D>(qu + row, g, qg[u]);
-        }
-#pragma unroll
-        for (int u = 0; u < kQGroup; ++u) {
-            const int tt = t0 + u * kWaves;
-            if (tt >= NT)
-                break;   // uniform
-            f4 glT[MT];   // lane (g,c): G_L^n[token 16tt+c][landmark 16kk+4g+i]
-            float ml = -INFINITY;
-#pragma unroll
-            for (int kk = 0; kk < MT; ++kk) {
-                f4 acc = {0.f, 0.f, 0.f, 0.f};
-                if constexpr (BFM) {
-                    acc = mfma_bf16(kbh[kk], qw[u], acc);
-                    acc = mfma_bf16(kbl[kk], qw[u], acc);
-                } else {
-#pragma unroll
-                    for (int s = 0; s < 8; ++s)
-                        acc = mfma4(kb[kk][s], qg[u][s], acc);
-                }
-                glT[kk] = acc;
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    if (16 * kk + 4 * g + i < m)
-                        ml = fmaxf(ml, acc[i]);
+            for (int u = 0; u < kQGroup; ++u) {
+                const int64_t row = int64_t(q0 + 16 * min(t0 + u * kWaves, NT - 1) + c) * d;
+                if constexpr (BFM)
+                    qw[u] = load_chunk8_bf8<D>(qu16 + row, g);
+                else
+                    load_chunk8<E, D>(qu + row, g, qg[u]);
             }
-            ml = a.s2 * max_groups(ml);
-            float od = 0.f;
 #pragma unroll
-            for (int kk = 0; kk < MT; ++kk)
+            for (int u = 0; u < kQGroup; ++u) {
+                const int tt = t0 + u * kWaves;
+                if (tt >= NT)
+                    break;   // uniform
+                f4 glT[MT];   // lane (g,c): G_L^n[token 16tt+c][landmark 16kk+4g+i]
+                float ml = -INFINITY;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float e = (16 * kk + 4 * g + i < m)
-                                        ? fast_exp2(fmaf(a.s2, glT[kk][i], -ml)) : 0.f;
-                    glT[kk][i] = e;
-                    od = fmaf(e, wdv[kk][i], od);
+                for (int kk = 0; kk < MT; ++kk) {
+                    f4 acc = {0.f, 0.f, 0.f, 0.f};
+                    if constexpr (BFM) {
+                        acc = mfma_bf16(kbh[kk], qw[u], acc);
+                        acc = mfma_bf16(kbl[kk], qw[u], acc);
+                    } else {
+#pragma unroll
+                        for (int s = 0; s < 8; ++s)
+                            acc = mfma4(kb[kk][s], qg[u][s], acc);
+                    }
+                    glT[kk] = acc;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        if (FULL || 16 * kk + 4 * g + i < m)
+                            ml = fmaxf(ml, acc[i]);
                 }
-            od = sum_groups(od);
-            const f4 odr = by_rows(od, vec, g, c);   // O_D of tokens 16tt + 4g + i
-            f4 rcp;
+                ml = a.s2 * max_groups(ml);
+                float od = 0.f;
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                rcp[i] = __builtin_amdgcn_rcpf(odr[i]);
-            bf8 gh[MP], gl[MP];
-            if constexpr (BFM) {
-#pragma unroll
-                for (int kp = 0; kp < MP; ++kp) {
-                    float g8[8];
+                for (int kk = 0; kk < MT; ++kk)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        g8[i] = glT[2 * kp][i];
-                        g8[4 + i] = (2 * kp + 1 < MT) ? glT[(2 * kp + 1) % MT][i] : 0.f;
+                        const float e = (FULL || 16 * kk + 4 * g + i < m)
+                                            ? fast_exp2(fmaf(a.s2, glT[kk][i], -ml)) : 0.f;
+                        glT[kk][i] = e;
+                        if constexpr (!kOnes)
+                            od = fmaf(e, wdv[kk][i], od);
                     }
-                    split_bf16(g8, gh[kp], gl[kp]);
-                }
-            }
+                f4 rcp;
+                if constexpr (!kOnes) {
+                    od = sum_groups(od);
+                    const f4 odr = by_rows(od, vec, g, c);   // O_D of tokens 16tt + 4g + i
 #pragma unroll
-            for (int ct = 0; ct < 2; ++ct) {
-                f4 on = {0.f, 0.f, 0.f, 0.f};
+                    for (int i = 0; i < 4; ++i)
+                        rcp[i] = __builtin_amdgcn_rcpf(odr[i]);
+                }
+                bf8 gh[MP], gl[MP];
                 if constexpr (BFM) {
 #pragma unroll
                     for (int kp = 0; kp < MP; ++kp) {
-                        on = mfma_bf16(gh[kp], wh[kp][ct], on);
-                        on = mfma_bf16(gh[kp], wl[kp][ct], on);
-                        on = mfma_bf16(gl[kp], wh[kp][ct], on);
-                    }
-                } else {
+                        float g8[8];
 #pragma unroll
-                    for (int kk = 0; kk < MT; ++kk)
-                        on = mm16_acc(glT[kk], WR[kk][ct], on);
+                        for (int i = 0; i < 4; ++i) {
+                            g8[i] = glT[2 * kp][i];
+                            g8[4 + i] = (2 * kp + 1 < MT) ? glT[(2 * kp + 1) % MT][i] : 0.f;
+                        }
+                        split_bf16(g8, gh[kp], gl[kp]);
+                    }
                 }
-                const int f = 16 * ct + c;
-                if (f < d) {
+                f4 on[NCT];
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) {
+                    f4 acc = {0.f, 0.f, 0.f, 0.f};
+                    if constexpr (BFM) {
+#pragma unroll
+                        for (int kp = 0; kp < MP; ++kp) {
+                            acc = mfma_bf16(gh[kp], wh[kp][ct], acc);
+                            acc = mfma_bf16(gh[kp], wl[kp][ct], acc);
+                            acc = mfma_bf16(gl[kp], wh[kp][ct], acc);
+                        }
+                    } else {
+#pragma unroll
+                        for (int kk = 0; kk < MT; ++kk)
+                            acc = mm16_acc(glT[kk], WR[kk][ct], acc);
+                    }
+                    on[ct] = acc;
+                }
+                if constexpr (kOnes) {   // O_D = column d of the last feature tile
 #pragma unroll
                     for (int i = 0; i < 4; ++i)
-                        E::store(ou, int64_t(q0 + 16 * tt + 4 * g + i) * d + f, on[i] * rcp[i]);
+                        rcp[i] = __builtin_amdgcn_rcpf(row_bcast<D % 16>(on[NCT - 1][i]));
                 }
+                // The tile of O, row-major as in memory, to the stage.
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) {
+                    const int f = 16 * ct + c;
+                    if (f < d) {
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const float x = on[ct][i] * rcp[i];
+                            if constexpr (E::bytes == 4)
+                                reinterpret_cast<float *>(stage)[(4 * g + i) * D + f] = x;
+                            else
+                                reinterpret_cast<uint16_t *>(stage)[(4 * g + i) * D + f] =
+                                    uint16_t(cvt_bf16x2(x, 0.f));
+                        }
+                    }
+                }
+                wave_sync();
+                f4 *dst = reinterpret_cast<f4 *>(ob + int64_t(q0 + 16 * tt) * d * E::bytes);
+                const f4 *src = reinterpret_cast<const f4 *>(stage);
+#pragma unroll
+                for (int p0 = 0; p0 < kPieces; p0 += 64)
+                    if (p0 + lane < kPieces)
+                        dst[p0 + lane] = src[p0 + lane];
+                wave_sync();
             }
         }
-    }
+    };
+    if (m == 16 * MT)
+        tiles(Flag<true>{});
+    else
+        tiles(Flag<false>{});
 }
 
 // ---- host side ----------------------------------------------------------------
@@ -626,7 +730,7 @@ void launch_split_md(const Problem &p, const Plan &s, const SplitArgs &a, hipStr
     const dim3 block(64 * kWaves);
     hipLaunchKernelGGL((split_pool_kernel<E, D>), dim3(U * unsigned(p.m * s.pieces)), block, 0,
                        stream, q, k, a);
-    hipLaunchKernelGGL(split_bar_kernel, dim3(U), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(split_bar_kernel, dim3(U * 2 * kLm), dim3(64), 0, stream, a);
     const bool bfm = E::bytes == 2 && p.N % 32 == 0;
     if (bfm)
         hipLaunchKernelGGL((split_keys_kernel<E, MT, D, E::bytes == 2>),
@@ -678,7 +782,7 @@ void launch_split_e(const Problem &p, const Plan &s, const SplitArgs &a, hipStre
 
 bool split_supported(const Problem &p)
 {
-    if (p.N % 16 != 0 || p.m > 64 || !tiled_width(p.d))
+    if (p.N % 16 != 0 || p.m > 64 || !tiled_width(p.d) || uintptr_t(p.o) % 16 != 0)
         return false;
     if (p.dtype == 1) {   // 16-byte row pieces of bf16 need 4-byte aligned rows
         const uintptr_t mis = uintptr_t(p.q) | uintptr_t(p.k) | uintptr_t(p.v);

@@ -60,16 +60,6 @@ __device__ inline f4 mfma_bf16(bf8 a, bf8 b, f4 c)
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-__device__ inline void split_bf16(const float (&x)[8], bf8 &hi, bf8 &lo)
-{
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        const __bf16 h = (__bf16)x[j];
-        hi[j] = h;
-        lo[j] = (__bf16)(x[j] - (float)h);
-    }
-}
-
 struct __attribute__((aligned(4))) U16B {
     uint32_t w[4];
 };
@@ -87,6 +77,22 @@ __device__ inline uint32_t cvt_bf16x2(float lo, float hi)
     typedef float f2 __attribute__((ext_vector_type(2)));
     typedef __bf16 b2 __attribute__((ext_vector_type(2)));
     return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2{lo, hi}), b2));   // RNE
+}
+
+// Eight fp32 values as hi = bf16(x) and lo = bf16(x - hi), both rounded to
+// nearest even, converted in pairs.
+__device__ inline void split_bf16(const float (&x)[8], bf8 &hi, bf8 &lo)
+{
+    U16B h, l;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        h.w[p] = cvt_bf16x2(x[2 * p], x[2 * p + 1]);
+        const float h0 = __uint_as_float(h.w[p] << 16);
+        const float h1 = __uint_as_float(h.w[p] & 0xffff0000u);
+        l.w[p] = cvt_bf16x2(x[2 * p] - h0, x[2 * p + 1] - h1);
+    }
+    hi = __builtin_bit_cast(bf8, h);
+    lo = __builtin_bit_cast(bf8, l);
 }
 
 __device__ inline SplitTile split_tile(f4 x)

@@ -223,6 +223,8 @@ def test_forward_ws_validation(L):
     assert f(o=q + 64) == EOVERLAP
     assert f(N=4095) == ESHAPE
     assert f(opts=B.make_opts(variant=5)) == EARG
+    # the token-split kernels store O in 16-byte pieces
+    assert f(opts=B.make_opts(variant=B.VARIANT_SPLIT), o=o + 4) == EUNSUP
     assert f(opts=B.make_opts(variant=B.VARIANT_SPLIT), N=4096 + 16) == ESHAPE  # no 2-D grid
     assert L.nystra_attn_forward_ws(None, None, None, None, 0, 2, N, d, m, 0, None, None, 0,
                                     None) == OK
