@@ -128,8 +128,8 @@ int nystra_attn_forward_ex(const void *Q, const void *K, const void *V, void *O,
  * nystra_attn_forward_ws needs for these arguments: 0 unless the call would
  * run the token-split kernels.  AUTO chooses them when the shape is supported
  * (N % 16 == 0, d_h in {8, 16, 24, 30, 32}, m <= 64; for bf16, Q, K, V 4-byte
- * aligned) and the units are too few for one workgroup per unit to fill the
- * GPU; NYSTRA_VARIANT_SPLIT forces them.  The size depends on the arguments
+ * aligned; O 16-byte aligned) and N >= 4096, or N >= 2048 with fewer than 512
+ * units; NYSTRA_VARIANT_SPLIT forces them.  The size depends on the arguments
  * only, not on any pointer (aligned tensors are assumed), and is about
  * units x (N / chunk) x 8.7 KB for key chunks of 256..4096 tokens.  Host-only.
  *

@@ -107,9 +107,14 @@ int finish_launch(hipError_t e)
     return NYSTRA_OK;
 }
 
-// Token-split kernels pay off when one workgroup per unit would leave the GPU
-// short of work: few units with long windows.
-bool split_preferred(const Problem &p) { return p.units < 512 && p.N >= 2048; }
+// Token-split kernels pay off for long windows: from 64 x 64 tokens on they beat
+// one workgroup per unit at every unit count measured (384 to 1536 units),
+// from 2048 tokens when the units are too few to fill the GPU (< 512).  At
+// 32 x 32 windows with 1536 units the one-pass kernel is faster.
+bool split_preferred(const Problem &p)
+{
+    return p.N >= 4096 || (p.N >= 2048 && p.units < 512);
+}
 
 // Resolves options and the problem; does not touch device memory.  with_ws
 // says whether the entry point takes a workspace (and so may run the

@@ -31,7 +31,10 @@ using namespace core;
 
 constexpr int kWP = 32;                    // pitch (floats) of feature rows in the workspace
 constexpr int kLm = 64;                    // landmark rows reserved per unit
-constexpr int kRecT = kLm * kWP;           // record: T rows, then T_D, then the row maxima
+// Chunk record of pass B: T by column groups of four ([kWP / 4][kLm][4], so a
+// merge block reads one contiguous piece per chunk), then T_D, then the row
+// maxima.  The merged record of pass C has T row-major ([kLm][kWP]) instead.
+constexpr int kRecT = kLm * kWP;
 constexpr int kRecD = kRecT;
 constexpr int kRecM = kRecT + kLm;
 constexpr int kRec = kRecT + 2 * kLm;
@@ -51,7 +54,7 @@ struct SplitArgs {
     int nqchunk, qchunk_len;   // pass D: query chunks per unit, queries per chunk
     float *part;   // [units][2][m * pieces][kWP]  piece sums of Q, then K
     float *bar;    // [units][2][kLm][kWP]         Qbar, then Kbar (zero past m, d)
-    float *rec;    // [units][nchunk][kRec]        chunk records of pass B
+    float *rec;    // [units][nchunk][kRec]        chunk records of pass B (T by column groups)
     float *comb;   // [units][kRec]                merged T, T_D and s2 * m_U
     float *wout;   // [units][kWout]               W and W_D
 };
@@ -361,7 +364,7 @@ split_keys_kernel(const typename E::T *__restrict__ k, const typename E::T *__re
             acc += fw * *reinterpret_cast<const f4 *>(&recs[v][l * kWP + f]);
             den += fw * recs[v][kOnes ? l * kWP + d : LD + l];
         }
-        *reinterpret_cast<f4 *>(out + l * kWP + f) = acc;
+        *reinterpret_cast<f4 *>(out + (f >> 2) * (kLm * 4) + 4 * l) = acc;
         if (f == 0) {
             out[kRecD + l] = den;
             out[kRecM + l] = mx;
@@ -387,7 +390,8 @@ __global__ void __launch_bounds__(256) split_merge_kernel(SplitArgs a, int MT)
     const int slice = threadIdx.x >> 6, t = threadIdx.x & 63;
     const int li = t >> 2, x = t & 3;
     const int l = 16 * j + li;
-    const int col = q < kMergeGroups - 1 ? l * kWP + 4 * q + x : kRecD + l;
+    const int col = q < kMergeGroups - 1 ? q * (kLm * 4) + 4 * l + x : kRecD + l;   // in a record
+    const int dst = q < kMergeGroups - 1 ? l * kWP + 4 * q + x : kRecD + l;         // merged
     const float *rec = a.rec + unit * a.nchunk * kRec;
     float mx = -INFINITY, sum = 0.f;
     int ch = slice;
@@ -428,7 +432,7 @@ __global__ void __launch_bounds__(256) split_merge_kernel(SplitArgs a, int MT)
         for (int s = 0; s < 4; ++s)   // a slice without chunks has max -inf and weight 0
             tot += fast_exp2(a.s2 * (smax[s][t] - M)) * ssum[s][t];
         float *cb = a.comb + unit * kRec;
-        cb[col] = tot;
+        cb[dst] = tot;
         if (q == 0 && x == 0)
             cb[kRecM + l] = a.s2 * M;
     }
