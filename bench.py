@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--sweep-n", default="64,256,1024,4096")
     ap.add_argument("--sweep-m", default="8,16,32,64")
     ap.add_argument("--sweep-k", default="1,3,4,5,6")
+    ap.add_argument("--block", default=None,
+                    help="comma-separated block layers to time (swinir, uformer, win16, win32, "
+                         "global) or 'all': the window-attention block with PnP-Nystra vs exact")
     ap.add_argument("--sweep-side", type=int, default=512,
                     help="side of the square feature map the sweep cuts into windows")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -249,6 +252,86 @@ def sweep(args):
     return 0
 
 
+# Window-attention block layers (the c2-c5 layers as whole blocks, and one
+# global window): (map side, channels, heads, window, m).
+BLOCK_LAYERS = {
+    "swinir": (256, 180, 6, 8, 16),    # c2: 8x8 windows, 6 heads of 30
+    "uformer": (512, 32, 1, 8, 8),     # c3: 8x8 windows, 1 head of 32
+    "win16": (512, 180, 6, 16, 32),    # c4: 16x16 windows
+    "win32": (512, 256, 8, 32, 64),    # c5: 32x32 windows, 8 heads of 32
+    "global": (512, 180, 6, 512, 64),  # one window per map
+}
+
+
+def block_bench(args):
+    """Per layer: one block call (QKV projection with window partition and a
+    shift of half a window, attention, head merge, output projection, window
+    reverse) with PnP-Nystra and with exact attention, the attention operator
+    alone on the same Q, K, V, and the projections' achieved rate."""
+    import torch
+    from paper_2506_08520_amd import binding as B
+    from paper_2506_08520_amd import workloads as W
+
+    B.lib()
+    names = list(BLOCK_LAYERS) if args.block == "all" else args.block.split(",")
+
+    def timed(fn, reps):
+        s = torch.cuda.current_stream()
+        fn()
+        r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        r0.record(s)
+        for _ in range(reps):
+            fn()
+        r1.record(s)
+        torch.cuda.synchronize()
+        return r0.elapsed_time(r1) / reps * 1e3   # us
+
+    for name in names:
+        side, C, heads, w, m = BLOCK_LAYERS[name]
+        shift = w // 2 if w < side else 0
+        dt = args.dtype
+        tdt = torch.float32 if dt == "f32" else torch.bfloat16
+        x, wq, bq, wp, bp = (torch.from_numpy(a).to(tdt).cuda()
+                             for a in W.block_inputs(1, side, side, C, seed=4242, dtype=dt))
+        code = B.F32 if dt == "f32" else B.BF16
+        shape = B.BlockShape(1, side, side, C, heads, w, shift)
+        y = torch.empty_like(x)
+        res = {"layer": name, "dtype": dt, "map": f"{side}x{side}x{C}", "heads": heads,
+               "window": w, "shift": shift, "m": m, "tokens": side * side}
+        reps = 20 if w < side else 5
+        for att, key in ((B.BLOCK_NYSTROM, "nystrom"), (B.BLOCK_EXACT, "exact")):
+            if key == "exact" and args.no_exact:
+                continue
+            nb = B.nystra_block_workspace_size(shape, m, code, None, att)
+            ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+            res[f"block_{key}_us"] = round(timed(lambda: B.nystra_block_forward(
+                x, wq, bq, wp, bp, heads, w, shift=shift, m=m, attention=att, workspace=ws,
+                out=y), reps if key == "nystrom" or w <= 32 else 3), 2)
+            del ws
+        # the attention alone on window-partitioned tensors of the same size
+        nw = (side // w) ** 2
+        q, k, v = (torch.randn(nw, heads, w * w, C // heads, device="cuda").to(tdt)
+                   for _ in range(3))
+        o = torch.empty_like(q)
+        na = B.nystra_attn_workspace_size(nw, heads, w * w, C // heads, m, code)
+        wsa = torch.empty(max(na, 1), dtype=torch.uint8, device="cuda")
+        res["attention_nystrom_us"] = round(timed(lambda: B.nystra_attn_forward_ws(
+            q, k, v, m, workspace=wsa, out=o), reps), 2)
+        if not args.no_exact:
+            res["attention_exact_us"] = round(timed(lambda: B.nystra_exact_attn_forward(
+                q, k, v, out=o), reps if w <= 32 else 3), 2)
+            res["block_speedup_vs_exact"] = round(res["block_exact_us"] / res["block_nystrom_us"], 3)
+        proj_us = res["block_nystrom_us"] - res["attention_nystrom_us"]
+        flops = 8.0 * side * side * C * C   # 2 rows C 3C + 2 rows C C
+        res["projections_us"] = round(proj_us, 2)
+        res["projections_tflops"] = round(flops / (proj_us * 1e-6) / 1e12, 1)
+        print(json.dumps(res), flush=True)
+        del x, wq, bq, wp, bp, y, q, k, v, o, wsa
+        torch.cuda.empty_cache()
+    return 0
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -258,6 +341,8 @@ def main():
         return 2
     if args.sweep:
         return sweep(args)
+    if args.block:
+        return block_bench(args)
     import torch
     from paper_2506_08520_amd import binding as B
     from paper_2506_08520_amd import workloads as W

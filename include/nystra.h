@@ -147,6 +147,47 @@ int nystra_attn_forward_ws(const void *Q, const void *K, const void *V, void *O,
                            const nystra_opts *opts, void *workspace, size_t workspace_bytes,
                            void *stream);
 
+/* Window-attention block around the operator: the structure of Sec. 1 for
+ * SwinIR / Uformer-style models, from a feature map X to a feature map Y.
+ *   1. the B x H x W map is rolled by -shift in both directions and cut into
+ *      (H / window) x (W / window) windows of N = window^2 tokens (windows
+ *      numbered image-major, then row-major; tokens row-major);
+ *   2. Q, K, V = X_win W_qkv + b_qkv (W_qkv [C][3C]: Q, K, V column blocks,
+ *      head j taking columns j d_h .. (j+1) d_h - 1 of each, d_h = C / heads);
+ *   3. per (window, head): PnP-Nystra (as nystra_attn_forward_ws, with m and
+ *      opts) or, with attention = NYSTRA_BLOCK_EXACT, exact softmax attention
+ *      (opts->scale only);
+ *   4. heads concatenated, Y_win = O W_proj + b_proj (W_proj [C][C]);
+ *   5. every token written back to its pixel (the roll undone).
+ * Relative-position bias and the shifted-window mask are not applied (they
+ * are not part of Eqs. (1)-(8)).
+ * X, Y: [batch][height][width][channels] DEVICE buffers in `dtype`; weights
+ * and biases in `dtype` (biases may be NULL: zero).  Q, K, V and the
+ * attention output are stored in `dtype` in the workspace (as a model in that
+ * dtype stores them); products accumulate in fp32 on the matrix cores.
+ * Limits: window divides height and width, 0 <= shift < window, heads
+ * divides channels, d_h <= 64, channels <= 4096, batch * height * width
+ * <= 2^31 - 1, and the attention limits above for N and m.
+ * nystra_block_workspace_size: host-only size of the workspace
+ * nystra_block_forward needs (Q, K, V, O and, for long windows, the
+ * token-split workspace).  nystra_block_forward: workspace as for
+ * nystra_attn_forward_ws (256-byte aligned, disjoint from every other
+ * argument, NYSTRA_ERR_WORKSPACE otherwise); Y must not overlap X, the
+ * weights or the biases. */
+typedef struct nystra_block_shape {
+    int batch, height, width, channels, heads, window, shift;
+} nystra_block_shape;
+
+typedef enum { NYSTRA_BLOCK_NYSTROM = 0, NYSTRA_BLOCK_EXACT = 1 } nystra_block_attention;
+
+int nystra_block_workspace_size(const nystra_block_shape *shape, int m, int dtype,
+                                const nystra_opts *opts, int attention, size_t *bytes);
+
+int nystra_block_forward(const void *X, const void *Wqkv, const void *bqkv, const void *Wproj,
+                         const void *bproj, void *Y, const nystra_block_shape *shape, int m,
+                         int dtype, const nystra_opts *opts, int attention, void *workspace,
+                         size_t workspace_bytes, void *stream);
+
 /* Exact windowed softmax self-attention, Eq. (1), per unit:
  *   O = softmax(scale Q K^T) V, with the row maximum subtracted inside the
  *   softmax.  scale <= 0 selects 1/sqrt(d_h).  Same layout, limits and

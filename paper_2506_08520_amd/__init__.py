@@ -11,6 +11,8 @@ from .binding import (  # noqa: F401
     nystra_attn_forward_ex,
     nystra_attn_forward_ws,
     nystra_attn_workspace_size,
+    nystra_block_forward,
+    nystra_block_workspace_size,
     nystra_exact_attn_forward,
     nystra_landmark_pool,
     nystra_landmark_map,

@@ -22,8 +22,10 @@ EXPORTS = (
     "nystra_default_opts", "nystra_attn_forward", "nystra_attn_forward_ex",
     "nystra_exact_attn_forward", "nystra_landmark_pool", "nystra_landmark_map",
     "nystra_select_variant", "nystra_attn_workspace_size", "nystra_attn_forward_ws",
+    "nystra_block_workspace_size", "nystra_block_forward",
     "nystra_status_str", "nystra_last_error",
 )
+BLOCK_NYSTROM, BLOCK_EXACT = 0, 1
 
 
 class NystraError(RuntimeError):
@@ -35,6 +37,11 @@ class NystraError(RuntimeError):
             if status == 7:
                 detail += ": " + _lib.nystra_last_error().decode()
         super().__init__(f"{where} failed with status {status} ({detail})")
+
+
+class BlockShape(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int) for n in ("batch", "height", "width", "channels", "heads",
+                                              "window", "shift")]
 
 
 class Opts(ctypes.Structure):
@@ -71,7 +78,13 @@ def lib():
     L.nystra_status_str.restype = ctypes.c_char_p
     L.nystra_last_error.argtypes = []
     L.nystra_last_error.restype = ctypes.c_char_p
-    for name in EXPORTS[:9]:
+    L.nystra_block_workspace_size.argtypes = [ctypes.POINTER(BlockShape), _i, _i,
+                                              ctypes.POINTER(Opts), _i,
+                                              ctypes.POINTER(ctypes.c_size_t)]
+    L.nystra_block_forward.argtypes = ([_vp] * 6 + [ctypes.POINTER(BlockShape), _i, _i,
+                                                     ctypes.POINTER(Opts), _i, _vp,
+                                                     ctypes.c_size_t, _vp])
+    for name in EXPORTS[:11]:
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -169,6 +182,42 @@ def nystra_attn_forward_ws(q, k, v, m, opts=None, workspace=None, out=None, stre
                                       po, _ptr(workspace), nbytes, _stream(stream))
     _check(rc, "nystra_attn_forward_ws")
     return o
+
+
+def nystra_block_workspace_size(shape, m, dtype=F32, opts=None, attention=BLOCK_NYSTROM):
+    n = ctypes.c_size_t(0)
+    po = ctypes.byref(opts) if opts is not None else None
+    _check(lib().nystra_block_workspace_size(ctypes.byref(shape), m, dtype, po, attention,
+                                             ctypes.byref(n)), "nystra_block_workspace_size")
+    return int(n.value)
+
+
+def nystra_block_forward(x, w_qkv, b_qkv, w_proj, b_proj, heads, window, shift=0, m=16,
+                         opts=None, attention=BLOCK_NYSTROM, workspace=None, out=None,
+                         stream=None):
+    """Window-attention block on x [B, H, W, C] (device, contiguous); returns Y
+    of the same shape.  Biases may be None.  The workspace is allocated from
+    torch's allocator when not given."""
+    import torch
+    if x.dim() != 4 or not x.is_contiguous() or not x.is_cuda:
+        raise ValueError("x must be a contiguous device tensor [B, H, W, C]")
+    for t in (w_qkv, b_qkv, w_proj, b_proj):
+        if t is not None and (t.dtype != x.dtype or not t.is_contiguous() or not t.is_cuda):
+            raise ValueError("weights must be contiguous device tensors of x's dtype")
+    Bn, H, W, C = (int(v) for v in x.shape)
+    shape = BlockShape(Bn, H, W, C, heads, window, shift)
+    code = _dtype_code(x)
+    need = nystra_block_workspace_size(shape, m, code, opts, attention)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+    nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    y = torch.empty_like(x) if out is None else out
+    po = ctypes.byref(opts) if opts is not None else None
+    rc = lib().nystra_block_forward(_ptr(x), _ptr(w_qkv), _ptr(b_qkv), _ptr(w_proj),
+                                    _ptr(b_proj), _ptr(y), ctypes.byref(shape), m, code, po,
+                                    attention, _ptr(workspace), nbytes, _stream(stream))
+    _check(rc, "nystra_block_forward")
+    return y
 
 
 def nystra_exact_attn_forward(q, k, v, scale=0.0, out=None, stream=None):

@@ -10,7 +10,7 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libnystra.so")
 OBJDIR = os.path.join(os.path.dirname(HERE), "_build")
 SOURCES = ["abi.hip", "generic.hip", "exact.hip", "tiled.hip", "tiled_large.hip",
-           "split.hip"]
+           "split.hip", "block.hip"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

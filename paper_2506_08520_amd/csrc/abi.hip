@@ -363,6 +363,162 @@ int nystra_select_variant(int N, int d_h, int m, int dtype, const nystra_opts *o
     return rc == NYSTRA_OK ? variant : -rc;
 }
 
+}  // extern "C"
+
+namespace {
+
+// Workspace layout of the block: Q, K, V, O, then the attention's own.
+struct BlockPlan {
+    Problem p;          // the attention problem on the workspace tensors
+    int variant;        // attention kernel family (Nystrom) or -1 (exact)
+    size_t qkvo_bytes;  // one of the four tensors, padded to 256 bytes
+    size_t bytes;       // total
+};
+
+size_t pad256(size_t x) { return (x + 255) & ~size_t(255); }
+
+int plan_block(const nystra_block_shape *s, int m, int dtype, const nystra_opts *opts,
+               int attention, BlockPlan *bp)
+{
+    if (!s)
+        return NYSTRA_ERR_NULL;
+    if (dtype != NYSTRA_F32 && dtype != NYSTRA_BF16)
+        return NYSTRA_ERR_DTYPE;
+    if (attention != NYSTRA_BLOCK_NYSTROM && attention != NYSTRA_BLOCK_EXACT)
+        return NYSTRA_ERR_ARG;
+    if (s->batch < 0 || s->height < 1 || s->width < 1 || s->window < 1 || s->heads < 1 ||
+        s->channels < 1 || s->channels > 4096 || s->channels % s->heads != 0 ||
+        s->height % s->window != 0 || s->width % s->window != 0 || s->shift < 0 ||
+        s->shift >= s->window || s->window > 1024)
+        return NYSTRA_ERR_SHAPE;
+    const int64_t rows = int64_t(s->batch) * s->height * s->width;
+    if (rows > int64_t(INT32_MAX) || !nystra::block_gemm_supported(rows, s->channels))
+        return NYSTRA_ERR_SHAPE;
+    const int64_t nw = int64_t(s->batch) * (s->height / s->window) * (s->width / s->window);
+    if (nw > int64_t(INT32_MAX))
+        return NYSTRA_ERR_SHAPE;
+    const int N = s->window * s->window, d = s->channels / s->heads;
+    int rc;
+    if (attention == NYSTRA_BLOCK_NYSTROM) {
+        rc = build_problem(nullptr, nullptr, nullptr, nullptr, int(nw), s->heads, N, d, m, dtype,
+                           opts, true, &bp->p, &bp->variant);
+    } else {
+        int64_t units = 0;
+        rc = check_common(int(nw), s->heads, N, d, dtype, &units);
+        if (rc == NYSTRA_OK && opts && !isfinite(opts->scale))
+            rc = NYSTRA_ERR_ARG;
+        bp->p = Problem{};
+        bp->p.units = units;
+        bp->p.N = N;
+        bp->p.d = d;
+        bp->p.dtype = dtype;
+        const float sc = opts ? opts->scale : 0.f;
+        bp->p.scale = sc > 0.f ? sc : float(1.0 / sqrt(double(d)));
+        bp->variant = -1;
+    }
+    if (rc != NYSTRA_OK)
+        return rc;
+    bp->qkvo_bytes = pad256(size_t(rows) * s->channels * dtype_bytes(dtype));
+    bp->bytes = 4 * bp->qkvo_bytes;
+    if (bp->variant == NYSTRA_VARIANT_SPLIT && bp->p.units > 0)
+        bp->bytes += nystra::split_workspace_bytes(bp->p);
+    return NYSTRA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int nystra_block_workspace_size(const nystra_block_shape *shape, int m, int dtype,
+                                const nystra_opts *opts, int attention, size_t *bytes)
+{
+    if (!bytes)
+        return NYSTRA_ERR_NULL;
+    BlockPlan bp;
+    const int rc = plan_block(shape, m, dtype, opts, attention, &bp);
+    if (rc != NYSTRA_OK)
+        return rc;
+    *bytes = shape->batch == 0 ? 0 : bp.bytes;
+    return NYSTRA_OK;
+}
+
+int nystra_block_forward(const void *X, const void *Wqkv, const void *bqkv, const void *Wproj,
+                         const void *bproj, void *Y, const nystra_block_shape *shape, int m,
+                         int dtype, const nystra_opts *opts, int attention, void *workspace,
+                         size_t workspace_bytes, void *stream)
+{
+    BlockPlan bp;
+    int rc = plan_block(shape, m, dtype, opts, attention, &bp);
+    if (rc != NYSTRA_OK)
+        return rc;
+    if (shape->batch == 0)
+        return NYSTRA_OK;
+    if (!X || !Wqkv || !Wproj || !Y)
+        return NYSTRA_ERR_NULL;
+    const int eb = dtype_bytes(dtype), C = shape->channels;
+    if (misaligned(X, eb) || misaligned(Wqkv, eb) || misaligned(Wproj, eb) || misaligned(Y, eb) ||
+        (bqkv && misaligned(bqkv, eb)) || (bproj && misaligned(bproj, eb)))
+        return NYSTRA_ERR_ALIGN;
+    const int64_t rows = int64_t(shape->batch) * shape->height * shape->width;
+    const int64_t xb = rows * C * eb, wqb = int64_t(C) * 3 * C * eb, wpb = int64_t(C) * C * eb;
+    if (overlaps(Y, xb, X, xb) || overlaps(Y, xb, Wqkv, wqb) || overlaps(Y, xb, Wproj, wpb) ||
+        (bqkv && overlaps(Y, xb, bqkv, 3 * C * eb)) || (bproj && overlaps(Y, xb, bproj, C * eb)))
+        return NYSTRA_ERR_OVERLAP;
+    if (!workspace || workspace_bytes < bp.bytes || misaligned(workspace, 256))
+        return NYSTRA_ERR_WORKSPACE;
+    const int64_t wsb = int64_t(bp.bytes);
+    if (overlaps(workspace, wsb, X, xb) || overlaps(workspace, wsb, Y, xb) ||
+        overlaps(workspace, wsb, Wqkv, wqb) || overlaps(workspace, wsb, Wproj, wpb) ||
+        (bqkv && overlaps(workspace, wsb, bqkv, 3 * C * eb)) ||
+        (bproj && overlaps(workspace, wsb, bproj, C * eb)))
+        return NYSTRA_ERR_WORKSPACE;
+    char *ws = static_cast<char *>(workspace);
+    void *q = ws, *k = ws + bp.qkvo_bytes, *v = ws + 2 * bp.qkvo_bytes,
+         *o = ws + 3 * bp.qkvo_bytes;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    nystra::BlockGemm g;
+    g.rows = rows;
+    g.H = shape->height;
+    g.W = shape->width;
+    g.C = C;
+    g.heads = shape->heads;
+    g.w = shape->window;
+    g.shift = shape->shift;
+    g.dtype = dtype;
+    g.proj = false;
+    g.a = X;
+    g.wt = Wqkv;
+    g.bias = bqkv;
+    g.out0 = q;
+    g.out1 = k;
+    g.out2 = v;
+    hipError_t e = nystra::launch_block_gemm(g, st);
+    if (e != hipSuccess)
+        return finish_launch(e);
+    Problem p = bp.p;
+    p.q = q;
+    p.k = k;
+    p.v = v;
+    p.o = o;
+    if (bp.variant == -1)
+        e = nystra::launch_exact(p, st);
+    else if (bp.variant == NYSTRA_VARIANT_SPLIT)
+        e = nystra::launch_split(p, ws + 4 * bp.qkvo_bytes, st);
+    else if (bp.variant == NYSTRA_VARIANT_TILED && nystra::tiled_supported(p))
+        e = nystra::launch_tiled_forward(p, st);
+    else
+        e = nystra::launch_generic_forward(p, st);
+    if (e != hipSuccess)
+        return finish_launch(e);
+    g.proj = true;
+    g.a = o;
+    g.wt = Wproj;
+    g.bias = bproj;
+    g.out0 = Y;
+    g.out1 = g.out2 = nullptr;
+    return finish_launch(nystra::launch_block_gemm(g, st));
+}
+
 const char *nystra_status_str(int status)
 {
     switch (status) {

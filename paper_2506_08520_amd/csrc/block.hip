@@ -1,0 +1,572 @@
+// Window-attention block around the PnP-Nystra operator, the structure of
+// Sec. 1 for SwinIR / Uformer-style models: the map is cut into w x w windows
+// (after a cyclic shift s for shifted windows), Q, K, V = X W_qkv + b per
+// token, every (window, head) attends, the heads are concatenated, and
+// Y = O W_proj + b goes back to the token's pixel.
+//
+// Two launches of one MFMA GEMM surround the attention kernels:
+//   QKV   rows = tokens in window order, A row r = the pixel of token r in X;
+//         the epilogue writes Q, K, V straight into [window][head][N][d_h].
+//   PROJ  A row r = token r's d_h-wide slices of O, one per head (the head
+//         concatenation is a gather); the epilogue writes Y at the pixel.
+// A workgroup computes a 64 x 64 tile of the product over 32-deep chunks of
+// the contraction staged in LDS, the next chunk's loads in flight while the
+// current one is multiplied; four waves each own a 32 x 32 quarter (2 x 2
+// MFMA tiles).  Blocks are mapped so that the column tiles of one row tile
+// run on the same XCD and share its L2 for the gathered rows.
+#include "internal.hpp"
+#include "tile_common.hpp"
+
+namespace nystra {
+namespace {
+
+using namespace tile;
+
+constexpr int kBM = 64, kBN = 64, kBK = 32;
+
+struct BlockArgs {
+    int64_t rows;                 // tokens, B H W
+    int H, W, C, heads, dh, w, N, shift, nwx, nwy;
+    int ncols;                    // 3C (QKV) or C (PROJ)
+    int rtiles, ctiles;           // tile grid
+    const void *a;                // X (QKV) or O (PROJ)
+    const void *wt;               // [C][ncols]
+    const void *bias;             // [ncols] or null
+    void *out0, *out1, *out2;     // Q, K, V (QKV) or Y (PROJ)
+};
+
+// Flat pixel (b H + y) W + x of token t of window `win`.
+__device__ inline int64_t pixel_of(const BlockArgs &a, int64_t win, int t)
+{
+    const int per = a.nwy * a.nwx;
+    const int64_t b = win / per;
+    const int wi = int(win - b * per);
+    const int wy = wi / a.nwx, wx = wi - wy * a.nwx;
+    const int ty = t / a.w, tx = t - ty * a.w;
+    int y = wy * a.w + ty + a.shift, x = wx * a.w + tx + a.shift;
+    if (y >= a.H)
+        y -= a.H;
+    if (x >= a.W)
+        x -= a.W;
+    return (b * a.H + y) * a.W + x;
+}
+
+// Block id -> (row tile, column tile), so that consecutive logical tiles (the
+// column tiles of one row tile) land on one XCD (ids go round-robin over 8).
+__device__ inline void tile_of(const BlockArgs &a, int &rt, int &ct)
+{
+    const int T = a.rtiles * a.ctiles, q = T / 8, r = T % 8;
+    const int b = int(blockIdx.x), x = b % 8, local = b / 8;
+    const int L = (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + local;
+    rt = L / a.ctiles;
+    ct = L - rt * a.ctiles;
+}
+
+template <class E>
+__device__ inline float ld(const void *p, int64_t i)
+{
+    return E::load(static_cast<const typename E::T *>(p), i);
+}
+
+template <class E, bool PROJ>
+__global__ void __launch_bounds__(256) block_gemm_kernel(BlockArgs a)
+{
+    constexpr bool BF = E::bytes == 2;
+    // fp32: A [64][36], B [32][68] floats.  bf16: A [64][40], B^T [64][40] halves.
+    constexpr int PA = BF ? kBK + 8 : kBK + 4, PB = BF ? kBK + 8 : kBN + 4;
+    __shared__ __align__(16) typename E::T As[kBM * PA];
+    __shared__ __align__(16) typename E::T Bs[BF ? kBN * PB : kBK * PB];
+    int rt, ct;
+    tile_of(a, rt, ct);
+    const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, c = lane & 15;
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6), wr = wv >> 1, wc = wv & 1;
+    const int64_t m0 = int64_t(rt) * kBM;
+    const int n0 = ct * kBN;
+
+    // This thread's A row (fixed over the contraction) and B row of a chunk.
+    const int arow = tid >> 2, ak = (tid & 3) * 8;
+    const int64_t r = m0 + arow;
+    const bool rok = r < a.rows;
+    const int64_t win = rok ? r / a.N : 0;
+    const int t = rok ? int(r - win * a.N) : 0;
+    int64_t abase;   // QKV: element offset of the pixel row; PROJ: of head 0's slice
+    if constexpr (PROJ)
+        abase = (win * a.heads * a.N + t) * int64_t(a.dh);
+    else
+        abase = pixel_of(a, win, t) * int64_t(a.C);
+    const int64_t headstride = int64_t(a.N) * a.dh;
+    const int bk = tid >> 3, bn = (tid & 7) * 8;
+
+    float ra[8], rb[8];
+    auto fetch = [&](int k0) {
+        int k = k0 + ak;
+        int hh = 0, dd = 0;
+        if constexpr (PROJ) {
+            hh = k / a.dh;
+            dd = k - hh * a.dh;
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            float x = 0.f;
+            if (rok && k < a.C) {
+                if constexpr (PROJ)
+                    x = ld<E>(a.a, abase + hh * headstride + dd);
+                else
+                    x = ld<E>(a.a, abase + k);
+            }
+            ra[j] = x;
+            ++k;
+            if constexpr (PROJ) {
+                if (++dd == a.dh) {
+                    dd = 0;
+                    ++hh;
+                }
+            }
+        }
+        const int kb = k0 + bk;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int n = n0 + bn + j;
+            rb[j] = (kb < a.C && n < a.ncols) ? ld<E>(a.wt, int64_t(kb) * a.ncols + n) : 0.f;
+        }
+    };
+    auto stash = [&]() {
+        if constexpr (BF) {
+            U16B u;
+#pragma unroll
+            for (int p = 0; p < 4; ++p)
+                u.w[p] = cvt_bf16x2(ra[2 * p], ra[2 * p + 1]);   // exact: bf16 values
+            *reinterpret_cast<U16B *>(&As[arow * PA + ak]) = u;
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                Bs[(bn + j) * PB + bk] = uint16_t(cvt_bf16x2(rb[j], 0.f));
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                As[arow * PA + ak + j] = ra[j];
+                Bs[bk * PB + bn + j] = rb[j];
+            }
+        }
+    };
+
+    f4 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+        acc[i][0] = acc[i][1] = f4{0.f, 0.f, 0.f, 0.f};
+    fetch(0);
+    stash();
+    __syncthreads();
+    for (int k0 = 0; k0 < a.C; k0 += kBK) {
+        const bool more = k0 + kBK < a.C;   // uniform
+        if (more)
+            fetch(k0 + kBK);
+        if constexpr (BF) {
+#pragma unroll
+            for (int ti = 0; ti < 2; ++ti) {
+                const bf8 av = *reinterpret_cast<const bf8 *>(&As[(32 * wr + 16 * ti + c) * PA + 8 * g]);
+#pragma unroll
+                for (int tj = 0; tj < 2; ++tj) {
+                    const bf8 bv =
+                        *reinterpret_cast<const bf8 *>(&Bs[(32 * wc + 16 * tj + c) * PB + 8 * g]);
+                    acc[ti][tj] = mfma_bf16(av, bv, acc[ti][tj]);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int s = 0; s < kBK / 4; ++s) {
+                float av[2], bv[2];
+#pragma unroll
+                for (int i = 0; i < 2; ++i) {
+                    av[i] = As[(32 * wr + 16 * i + c) * PA + 4 * s + g];
+                    bv[i] = Bs[(4 * s + g) * PB + 32 * wc + 16 * i + c];
+                }
+#pragma unroll
+                for (int ti = 0; ti < 2; ++ti)
+#pragma unroll
+                    for (int tj = 0; tj < 2; ++tj)
+                        acc[ti][tj] = mfma4(av[ti], bv[tj], acc[ti][tj]);
+            }
+        }
+        __syncthreads();
+        if (more) {
+            stash();
+            __syncthreads();
+        }
+    }
+
+    // Epilogue: lane (g, c) holds rows 4g + i, column c of each 16 x 16 tile.
+#pragma unroll
+    for (int tj = 0; tj < 2; ++tj) {
+        const int n = n0 + 32 * wc + 16 * tj + c;
+        if (n >= a.ncols)
+            continue;
+        const float bias = a.bias ? ld<E>(a.bias, n) : 0.f;
+        int which = 0, hh = 0, dd = n;
+        if constexpr (!PROJ) {
+            which = n / a.C;
+            const int cc = n - which * a.C;
+            hh = cc / a.dh;
+            dd = cc - hh * a.dh;
+        }
+        typename E::T *dst = static_cast<typename E::T *>(which == 0 ? a.out0
+                                                          : which == 1 ? a.out1 : a.out2);
+#pragma unroll
+        for (int ti = 0; ti < 2; ++ti)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int64_t row = m0 + 32 * wr + 16 * ti + 4 * g + i;
+                if (row >= a.rows)
+                    continue;
+                const int64_t wn = row / a.N;
+                const int tt = int(row - wn * a.N);
+                const float v = acc[ti][tj][i] + bias;
+                if constexpr (PROJ)
+                    E::store(dst, pixel_of(a, wn, tt) * a.C + n, v);
+                else
+                    E::store(dst, ((wn * a.heads + hh) * a.N + tt) * int64_t(a.dh) + dd, v);
+            }
+    }
+}
+
+// Register-resident variant for C <= 256 (K padded to KP, a multiple of 32).
+// Each wave holds its 16 rows of A for the whole contraction in registers, in
+// the operand layout of the matrix cores: lane group g takes the contiguous
+// quarter k in [g KP/4, (g+1) KP/4), so A is read from memory exactly once.
+// The workgroup's eight waves (128 rows) stream W through LDS one 64-column
+// tile at a time, double-buffered: the next tile's loads are in flight while
+// the current one is multiplied.  W tiles in LDS: fp32 as [k][c][t] (the four
+// 16-column tiles' values of column c side by side, one 16-byte read per
+// step), bf16 transposed as [n][k] (eight k per 16-byte read).
+constexpr int kRkWaves = 8, kRkRows = 16 * kRkWaves;
+
+template <class E, int KP>
+struct RkLds {
+    static constexpr bool BF = E::bytes == 2;
+    static constexpr int PF = 68;            // fp32 [k][c][t]: 64 floats + 4 per k
+    static constexpr int PH = KP + 8;        // bf16 [n][k]: halves per column
+    static constexpr int tile = BF ? 64 * PH / 2 : KP * PF;   // floats per buffer
+    static constexpr int astage = 16 * 8 * (KP / (BF ? 2 : 1) + 4);   // 128 rows, words
+    static constexpr int total = 2 * tile > astage ? 2 * tile : astage;
+};
+
+template <class E, bool PROJ, int KP>
+__global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs a)
+{
+    constexpr bool BF = E::bytes == 2;
+    using L = RkLds<E, KP>;
+    constexpr int KQ = KP / 4;               // contraction slots per lane group
+    __shared__ __align__(16) float lds_all[L::total];
+    auto wbuf = [&](int b) { return lds_all + b * L::tile; };
+    const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, c = lane & 15;
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t m0 = int64_t(blockIdx.x) * kRkRows;
+
+    // ---- A: the workgroup's 128 rows are staged in LDS with coalesced 4-byte
+    // loads (lanes take consecutive words of a row; bf16 words hold two
+    // elements), then each lane copies its operand slots -- row 16 wv + c,
+    // k = g KQ + s -- into registers.  The stage shares LDS with the W tiles.
+    constexpr int EPW = BF ? 2 : 1;              // elements per 4-byte word
+    constexpr int AWL = KP / EPW;                // words per staged row
+    constexpr int AP = AWL + 4;                  // row pitch (words)
+    __shared__ int rowbase[kRkRows];             // element offset of row r (-1: none)
+    __shared__ int colofs[AWL];                  // element offset of word w in a row
+    float *astage = lds_all;
+    if (tid < kRkRows) {
+        const int64_t row = m0 + tid;
+        int base = -1;
+        if (row < a.rows) {
+            const int wn = int(row / a.N), tt = int(row - int64_t(wn) * a.N);
+            base = int(PROJ ? (int64_t(wn) * a.heads * a.N + tt) * a.dh
+                            : pixel_of(a, wn, tt) * a.C);
+        }
+        rowbase[tid] = base;
+    }
+    for (int w = tid; w < AWL; w += 64 * kRkWaves) {
+        const int k = w * EPW;
+        int off = k;
+        if constexpr (PROJ) {
+            const int hh = k / a.dh;
+            off = hh * a.N * a.dh + (k - hh * a.dh);
+        }
+        colofs[w] = k < a.C ? off : -1;
+    }
+    __syncthreads();
+    {
+        const uint32_t *src = static_cast<const uint32_t *>(a.a);
+        for (int j = tid; j < kRkRows * AWL; j += 64 * kRkWaves) {
+            const int row = j / AWL, w = j - row * AWL;
+            const int rb = rowbase[row], co = colofs[w];
+            const bool ok = rb >= 0 && co >= 0;
+            const int e = ok ? rb + co : 0;
+            const uint32_t x = src[BF ? e >> 1 : e];
+            reinterpret_cast<uint32_t *>(astage)[row * AP + w] = ok ? x : 0u;
+        }
+    }
+    __syncthreads();
+    float av[BF ? 1 : KQ];
+    bf8 ab[BF ? KQ / 8 : 1];
+    {
+        const float *arow = astage + (16 * wv + c) * AP;
+        if constexpr (BF) {
+#pragma unroll
+            for (int s = 0; s < KQ / 8; ++s)
+                ab[s] = *reinterpret_cast<const bf8 *>(arow + (g * KQ + 8 * s) / 2);
+        } else {
+#pragma unroll
+            for (int s = 0; s < KQ; s += 4) {
+                const f4 v = *reinterpret_cast<const f4 *>(arow + g * KQ + s);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    av[s + e] = v[e];
+            }
+        }
+    }
+    __syncthreads();   // the stage becomes the W tiles
+
+    // ---- W tiles: global -> registers -> LDS.  A thread gathers one column's
+    // values for several k (lanes take consecutive columns, so every load is
+    // coalesced) and writes them with one 16-byte LDS store: bf16 eight k of
+    // column n into [n][k]; fp32 the four 16-column tiles' values of column
+    // c at one k into [k][c][t].
+    constexpr int kPieces = BF ? KP * 8 : KP * 16;   // 16-byte LDS pieces of a tile
+    constexpr int kPer = (kPieces + 64 * kRkWaves - 1) / (64 * kRkWaves);
+    U16B wr[kPer];
+    const int nct = (a.ncols + 63) / 64;
+    const typename E::T *W = static_cast<const typename E::T *>(a.wt);
+    // Every load reads an in-bounds address (k and n clamped) and the padding
+    // (k >= C, n >= ncols) is zeroed by a select, so the loop has no branches.
+    // Offsets are 32-bit (the host keeps every tensor under 2^31 elements).
+    auto wfetch = [&](int ct) {
+        const int n0 = 64 * ct;
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) {
+            const int idx = tid + j * 64 * kRkWaves;
+            U16B u = {{0u, 0u, 0u, 0u}};
+            if (kPer * 64 * kRkWaves == kPieces || idx < kPieces) {
+                if constexpr (BF) {
+                    const int n = n0 + (idx & 63), k0 = 8 * (idx >> 6);
+                    const bool nok = n < a.ncols;
+                    const int nc = nok ? n : a.ncols - 1;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int k = k0 + e;
+                        const bool ok = nok && k < a.C;
+                        const uint32_t h =
+                            uint32_t(W[(k < a.C ? k : a.C - 1) * a.ncols + nc]);
+                        u.w[e >> 1] |= (ok ? h : 0u) << (16 * (e & 1));
+                    }
+                } else {
+                    const int cc = idx & 15, k = idx >> 4;
+                    const int kc = k < a.C ? k : a.C - 1;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int n = n0 + 16 * e + cc;
+                        const bool ok = k < a.C && n < a.ncols;
+                        const float x = W[kc * a.ncols + (n < a.ncols ? n : a.ncols - 1)];
+                        u.w[e] = ok ? __float_as_uint(x) : 0u;
+                    }
+                }
+            }
+            wr[j] = u;
+        }
+    };
+    auto wstash = [&](int buf) {
+        float *dst = wbuf(buf);
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) {
+            const int idx = tid + j * 64 * kRkWaves;
+            if (kPer * 64 * kRkWaves > kPieces && idx >= kPieces)
+                break;
+            if constexpr (BF)
+                *reinterpret_cast<U16B *>(reinterpret_cast<uint16_t *>(dst) +
+                                          (idx & 63) * L::PH + 8 * (idx >> 6)) = wr[j];
+            else
+                *reinterpret_cast<U16B *>(dst + (idx >> 4) * L::PF + 4 * (idx & 15)) = wr[j];
+        }
+    };
+    // Column part of the destination for the 64 columns of the current tile:
+    // which output tensor, and (QKV) head h, feature f -> h N d_h + f.
+    __shared__ int coltab[2][64];
+    __shared__ int colwhich[2][64];
+    auto cfill = [&](int ct, int buf) {
+        if (tid < 64) {
+            const int n = 64 * ct + tid;
+            int which = 0, col = n;
+            if constexpr (!PROJ) {
+                which = n / a.C;
+                const int cc = n - which * a.C;
+                const int hh = cc / a.dh;
+                col = hh * a.N * a.dh + (cc - hh * a.dh);
+            }
+            coltab[buf][tid] = col;
+            colwhich[buf][tid] = which;
+        }
+    };
+
+    // Row part of the destination of this lane's output rows 4g + i (-1: past
+    // the end): QKV (window wn, token tt) -> wn N C + tt d_h; PROJ -> pixel C.
+    int rowoff[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int row = int(m0) + 16 * wv + 4 * g + i;   // rows < 2^31
+        if (row >= a.rows) {
+            rowoff[i] = -1;
+            continue;
+        }
+        const int wn = row / a.N, tt = row - wn * a.N;
+        rowoff[i] = int(PROJ ? pixel_of(a, wn, tt) * a.C
+                             : int64_t(wn) * a.N * a.C + int64_t(tt) * a.dh);
+    }
+
+    // Workgroups start at different column tiles, so that at any moment they
+    // read different tiles of W instead of all hitting the same L2 lines.
+    const int start = int(blockIdx.x % unsigned(nct));
+    auto phys = [&](int i) { return i + start < nct ? i + start : i + start - nct; };
+    wfetch(phys(0));
+    wstash(0);
+    cfill(phys(0), 0);
+    __syncthreads();
+    for (int it = 0; it < nct; ++it) {
+        const int ct = phys(it);
+        const bool more = it + 1 < nct;   // uniform
+        if (more)
+            wfetch(phys(it + 1));
+        const float *wt = wbuf(it & 1);
+        f4 acc[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            acc[q] = f4{0.f, 0.f, 0.f, 0.f};
+        if constexpr (BF) {
+            const uint16_t *h = reinterpret_cast<const uint16_t *>(wt);
+#pragma unroll
+            for (int s = 0; s < KQ / 8; ++s)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const bf8 bv = *reinterpret_cast<const bf8 *>(
+                        &h[(16 * q + c) * L::PH + g * KQ + 8 * s]);
+                    acc[q] = mfma_bf16(ab[s], bv, acc[q]);
+                }
+        } else {
+#pragma unroll
+            for (int s = 0; s < KQ; ++s) {
+                const f4 bv = *reinterpret_cast<const f4 *>(&wt[(g * KQ + s) * L::PF + 4 * c]);
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    acc[q] = mfma4(av[s], bv[q], acc[q]);
+            }
+        }
+        // Epilogue: lane (g, c) holds rows 4g + i of the wave's 16, column c of tile q;
+        // destination = row part (per lane, computed once) + column part (table).
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int n = 64 * ct + 16 * q + c;
+            if (n >= a.ncols)
+                continue;
+            const float bias = a.bias ? ld<E>(a.bias, n) : 0.f;
+            const int col = coltab[it & 1][16 * q + c];
+            const int which = colwhich[it & 1][16 * q + c];
+            typename E::T *dst = static_cast<typename E::T *>(which == 0 ? a.out0
+                                                              : which == 1 ? a.out1 : a.out2);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (rowoff[i] >= 0) {
+                    const float v = acc[q][i] + bias;
+                    if constexpr (BF)
+                        dst[rowoff[i] + col] = uint16_t(cvt_bf16x2(v, 0.f));   // RNE
+                    else
+                        dst[rowoff[i] + col] = v;
+                }
+        }
+        if (more) {
+            wstash((it + 1) & 1);
+            cfill(phys(it + 1), (it + 1) & 1);
+        }
+        __syncthreads();
+    }
+}
+
+template <class E, bool PROJ, int KP>
+void launch_rk(const BlockArgs &a, hipStream_t stream)
+{
+    const unsigned blocks = unsigned((a.rows + kRkRows - 1) / kRkRows);
+    hipLaunchKernelGGL((block_gemm_rk_kernel<E, PROJ, KP>), dim3(blocks), dim3(64 * kRkWaves), 0,
+                       stream, a);
+}
+
+template <class E, bool PROJ>
+bool try_rk(const BlockArgs &a, hipStream_t stream)
+{
+    // 16-byte W pieces: fp32 rows 16-byte aligned, bf16 rows 4-byte aligned
+    if (a.rows * int64_t(a.C) >= (int64_t(1) << 31) ||
+        int64_t(a.C) * a.ncols >= (int64_t(1) << 31))
+        return false;   // 32-bit element offsets
+    const uintptr_t wp = uintptr_t(a.wt);
+    if (E::bytes == 4 ? (wp % 16 != 0 || a.ncols % 4 != 0) : (wp % 4 != 0 || a.ncols % 2 != 0))
+        return false;
+    // A as 4-byte words: bf16 needs an even C, and in PROJ an even d_h (a word
+    // never straddles two heads); the A base 4-byte aligned
+    if (uintptr_t(a.a) % 4 != 0 || (E::bytes == 2 && (a.C % 2 != 0 || (PROJ && a.dh % 2 != 0))))
+        return false;
+    if (a.C <= 32)
+        launch_rk<E, PROJ, 32>(a, stream);
+    else if (a.C <= 64)
+        launch_rk<E, PROJ, 64>(a, stream);
+    else if (a.C <= 128)
+        launch_rk<E, PROJ, 128>(a, stream);
+    else if (a.C <= 192)
+        launch_rk<E, PROJ, 192>(a, stream);
+    else if (a.C <= 256)
+        launch_rk<E, PROJ, 256>(a, stream);
+    else
+        return false;
+    return true;
+}
+
+template <class E, bool PROJ>
+void launch_gemm(const BlockArgs &a, hipStream_t stream)
+{
+    if (try_rk<E, PROJ>(a, stream))
+        return;
+    const unsigned blocks = unsigned(a.rtiles) * unsigned(a.ctiles);
+    hipLaunchKernelGGL((block_gemm_kernel<E, PROJ>), dim3(blocks), dim3(256), 0, stream, a);
+}
+
+}  // namespace
+
+bool block_gemm_supported(int64_t rows, int C)
+{
+    const int64_t rt = (rows + kBM - 1) / kBM, ct = (3 * int64_t(C) + kBN - 1) / kBN;
+    return rt * ct * 256 < (int64_t(1) << 32);
+}
+
+hipError_t launch_block_gemm(const BlockGemm &g, hipStream_t stream)
+{
+    BlockArgs a;
+    a.rows = g.rows;
+    a.H = g.H;
+    a.W = g.W;
+    a.C = g.C;
+    a.heads = g.heads;
+    a.dh = g.C / g.heads;
+    a.w = g.w;
+    a.N = g.w * g.w;
+    a.shift = g.shift;
+    a.nwx = g.W / g.w;
+    a.nwy = g.H / g.w;
+    a.ncols = g.proj ? g.C : 3 * g.C;
+    a.rtiles = int((g.rows + kBM - 1) / kBM);
+    a.ctiles = (a.ncols + kBN - 1) / kBN;
+    a.a = g.a;
+    a.wt = g.wt;
+    a.bias = g.bias;
+    a.out0 = g.out0;
+    a.out1 = g.out1;
+    a.out2 = g.out2;
+    if (g.dtype == 0)
+        g.proj ? launch_gemm<F32, true>(a, stream) : launch_gemm<F32, false>(a, stream);
+    else
+        g.proj ? launch_gemm<BF16, true>(a, stream) : launch_gemm<BF16, false>(a, stream);
+    return hipGetLastError();
+}
+
+}  // namespace nystra

@@ -52,6 +52,20 @@ bool split_supported(const Problem &p);
 size_t split_workspace_bytes(const Problem &p);
 hipError_t launch_split(const Problem &p, void *workspace, hipStream_t stream);
 
+// Projection GEMMs of the window-attention block.  QKV (proj = false): A rows
+// are the pixels of X in window order, outputs go to Q, K, V (out0..2) in
+// [window][head][N][d_h].  PROJ: A rows gather the heads of O, outputs go to
+// the pixels of Y (out0).  Weights are [C][3C] or [C][C]; bias may be null.
+struct BlockGemm {
+    int64_t rows;     // B H W
+    int H, W, C, heads, w, shift, dtype;
+    bool proj;
+    const void *a, *wt, *bias;
+    void *out0, *out1, *out2;
+};
+bool block_gemm_supported(int64_t rows, int C);
+hipError_t launch_block_gemm(const BlockGemm &g, hipStream_t stream);
+
 // Head widths with a tiled instantiation.
 inline bool tiled_width(int d) { return d == 8 || d == 16 || d == 24 || d == 30 || d == 32; }
 

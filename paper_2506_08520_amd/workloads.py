@@ -141,3 +141,17 @@ def iid(shape, seed, dtype="f32", std=1.0):
     """Plain i.i.d. N(0, std^2) Q, K, V of an arbitrary [..., N, d] shape."""
     rng = np.random.default_rng(seed)
     return tuple(round_to(std * rng.standard_normal(shape), dtype) for _ in range(3))
+
+
+def block_inputs(B, H, W, C, seed, dtype="f32", bias_std=0.02):
+    """Feature map and synthetic weights of one window-attention block:
+    x [B][H][W][C] ~ N(0, 1); W_qkv [C][3C] and W_proj [C][C] ~ N(0, 1/C)
+    (the scale of a trained block's projections); biases ~ N(0, bias_std^2).
+    Returns float64 arrays holding dtype-rounded values."""
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((B, H, W, C))
+    w_qkv = rng.standard_normal((C, 3 * C)) / np.sqrt(C)
+    b_qkv = bias_std * rng.standard_normal(3 * C)
+    w_proj = rng.standard_normal((C, C)) / np.sqrt(C)
+    b_proj = bias_std * rng.standard_normal(C)
+    return tuple(round_to(a, dtype) for a in (x, w_qkv, b_qkv, w_proj, b_proj))

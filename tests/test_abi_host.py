@@ -228,3 +228,60 @@ def test_forward_ws_validation(L):
     assert f(opts=B.make_opts(variant=B.VARIANT_SPLIT), N=4096 + 16) == ESHAPE  # no 2-D grid
     assert L.nystra_attn_forward_ws(None, None, None, None, 0, 2, N, d, m, 0, None, None, 0,
                                     None) == OK
+
+
+def bshape(**kw):
+    d = dict(batch=1, height=16, width=16, channels=96, heads=3, window=8, shift=0)
+    d.update(kw)
+    return B.BlockShape(*(d[k] for k in ("batch", "height", "width", "channels", "heads",
+                                         "window", "shift")))
+
+
+def test_block_workspace_size():
+    one = 16 * 16 * 96 * 4                      # one of Q, K, V, O in fp32 (256-byte multiple)
+    assert B.nystra_block_workspace_size(bshape(), 16) == 4 * one
+    assert B.nystra_block_workspace_size(bshape(), 16, B.BF16) == 2 * one
+    assert B.nystra_block_workspace_size(bshape(shift=4), 16, attention=B.BLOCK_EXACT) == 4 * one
+    assert B.nystra_block_workspace_size(bshape(batch=0), 16) == 0
+    # a whole-map window takes the token-split attention, whose workspace comes on top
+    glob = bshape(height=128, width=128, channels=64, heads=2, window=128)
+    assert B.nystra_block_workspace_size(glob, 64) > 4 * 128 * 128 * 64 * 4
+    for kw, status in [(dict(window=6), ESHAPE), (dict(shift=8), ESHAPE), (dict(shift=-1), ESHAPE),
+                       (dict(channels=100), ESHAPE), (dict(heads=0), ESHAPE),
+                       (dict(channels=4104, heads=3), ESHAPE), (dict(height=0), ESHAPE)]:
+        with pytest.raises(B.NystraError) as e:
+            B.nystra_block_workspace_size(bshape(**kw), 16)
+        assert e.value.status == status, kw
+    for args, status in [((16, 5), EDTYPE), ((3, 0), ESHAPE)]:
+        with pytest.raises(B.NystraError) as e:
+            B.nystra_block_workspace_size(bshape(), *args)
+        assert e.value.status == status
+    with pytest.raises(B.NystraError) as e:
+        B.nystra_block_workspace_size(bshape(), 16, attention=2)
+    assert e.value.status == EARG
+    n = ctypes.c_size_t(0)
+    assert B.lib().nystra_block_workspace_size(None, 16, 0, None, 0, ctypes.byref(n)) == ENULL
+    assert B.lib().nystra_block_workspace_size(ctypes.byref(bshape()), 16, 0, None, 0,
+                                               None) == ENULL
+
+
+def test_block_forward_validation(L):
+    s = bshape()
+    need = B.nystra_block_workspace_size(s, 16)
+    x, wq, wp, y, ws = P, P + (1 << 24), P + (2 << 24), P + (3 << 24), P + (4 << 24)
+
+    def f(x=x, wq=wq, bq=None, wp=wp, bp=None, y=y, ws=ws, nb=need, s=s, dtype=0):
+        return L.nystra_block_forward(x, wq, bq, wp, bp, y, ctypes.byref(s), 16, dtype, None, 0,
+                                      ws, nb, None)
+
+    assert f(x=None) == ENULL
+    assert f(wp=None) == ENULL
+    assert f(x=x + 2) == EALIGN
+    assert f(bq=wq + (1 << 20) + 2) == EALIGN
+    assert f(y=x + 64) == EOVERLAP
+    assert f(y=wq - 256) == EOVERLAP          # Y's tail meets W_qkv
+    assert f(ws=None) == EWS
+    assert f(nb=need - 1) == EWS
+    assert f(ws=ws + 64) == EWS
+    assert f(ws=y) == EWS
+    assert f(s=bshape(batch=0), x=None, y=None, ws=None) == OK

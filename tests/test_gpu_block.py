@@ -1,0 +1,80 @@
+"""GPU parity of the window-attention block (nystra_block_forward) against
+the float64 block oracle: projections, window partition with cyclic shift,
+head split and merge, window reverse, around PnP-Nystra or exact attention.
+Bars: fp32 max-abs <= 1e-4; bf16 max-abs <= 2e-2 x RMS after allowing every
+element the half bf16 ulp that storing it costs.  A bf16 block stores three
+times (Q/K/V, the attention output, Y), and the GPU rounds fp32 values where
+the oracle rounds float64 ones, so an element within fp32 noise of a rounding
+boundary may land one bf16 ulp away; on Y's heavy tail one ulp is already
+~2% of RMS."""
+import numpy as np
+import pytest
+
+from oracle import block as OB
+from paper_2506_08520_amd import binding as B
+from paper_2506_08520_amd import workloads as W
+from helpers import TOL, error, to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def run_block(inputs, heads, window, shift, m, dtype, attention, mode=0, iters=6, nobias=False):
+    x, wq, bq, wp, bp = (to_dev(a, dtype) for a in inputs)
+    if nobias:
+        bq = bp = None
+    opts = B.make_opts(pinv_iters=iters, landmark_mode=mode)
+    att = B.BLOCK_NYSTROM if attention == "nystrom" else B.BLOCK_EXACT
+    y = B.nystra_block_forward(x, wq, bq, wp, bp, heads, window, shift=shift, m=m, opts=opts,
+                               attention=att)
+    torch.cuda.synchronize()
+    return to_host(y)
+
+
+# (B, H, W, C, heads, window, shift, m, dtype, attention)
+CASES = [
+    (1, 32, 32, 180, 6, 8, 0, 16, "f32", "nystrom"),    # SwinIR-shaped (c2 layer, smaller map)
+    (1, 32, 32, 180, 6, 8, 4, 16, "f32", "nystrom"),    # shifted windows
+    (2, 24, 16, 180, 6, 8, 4, 16, "bf16", "nystrom"),
+    (1, 32, 32, 32, 1, 8, 4, 8, "bf16", "nystrom"),     # Uformer-shaped (c3)
+    (1, 32, 48, 180, 6, 16, 8, 32, "f32", "nystrom"),   # 16 x 16 windows (c4)
+    (1, 64, 64, 256, 8, 32, 16, 64, "bf16", "nystrom"), # 32 x 32 windows (c5)
+    # 240 tokens: ragged row tile, d_h = 8.  (m = 4 here is so ill-conditioned
+    # that fp32-sized input noise moves the float64 oracle by 4e-5 at outputs
+    # of 19; m = 8 is not.)
+    (1, 12, 20, 24, 3, 4, 2, 8, "f32", "nystrom"),
+    (1, 16, 16, 60, 3, 8, 3, 16, "f32", "nystrom"),     # d_h = 20: generic attention kernel
+    (2, 16, 16, 96, 3, 8, 4, 0, "f32", "exact"),
+    (1, 16, 16, 180, 6, 16, 8, 0, "bf16", "exact"),
+    (1, 64, 64, 64, 2, 64, 0, 64, "f32", "nystrom"),    # one window per map: token-split path
+    (1, 64, 64, 64, 2, 64, 32, 16, "bf16", "nystrom"),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "x".join(map(str, c)))
+def test_block_parity(case):
+    Bn, H, Wd, C, heads, w, s, m, dtype, att = case
+    inputs = W.block_inputs(Bn, H, Wd, C, seed=H * Wd + C + s, dtype=dtype)
+    ref = OB.block_forward(*inputs, heads=heads, window=w, shift=s, m=max(m, 1), attention=att,
+                           dtype=dtype)
+    got = run_block(inputs, heads, w, s, m, dtype, att)
+    err = error(got, ref, dtype, storage_floor=dtype == "bf16")
+    print(f"{case}: error {err:.3e} (literal {error(got, ref, dtype):.3e})")
+    assert err <= TOL[dtype]
+
+
+def test_block_without_biases_and_segment_pooling():
+    inputs = W.block_inputs(1, 16, 16, 96, seed=77, dtype="f32")
+    x, wq, _, wp, _ = inputs
+    zq, zp = np.zeros(3 * 96), np.zeros(96)
+    ref = OB.block_forward(x, wq, zq, wp, zp, heads=3, window=8, shift=2, m=8, mode=1)
+    got = run_block(inputs, 3, 8, 2, 8, "f32", "nystrom", mode=1, nobias=True)
+    assert error(got, ref, "f32") <= TOL["f32"]
+
+
+def test_block_deterministic():
+    inputs = W.block_inputs(1, 32, 32, 180, seed=5, dtype="f32")
+    a = run_block(inputs, 6, 8, 4, 16, "f32", "nystrom")
+    b = run_block(inputs, 6, 8, 4, 16, "f32", "nystrom")
+    assert np.array_equal(a, b)
