@@ -322,6 +322,24 @@ def block_bench(args):
             res["attention_exact_us"] = round(timed(lambda: B.nystra_exact_attn_forward(
                 q, k, v, out=o), reps if w <= 32 else 3), 2)
             res["block_speedup_vs_exact"] = round(res["block_exact_us"] / res["block_nystrom_us"], 3)
+        # the SwinIR-shaped transformer block (LayerNorm, window attention,
+        # residual, LayerNorm, MLP of ratio 2, residual) with each attention
+        from paper_2506_08520_amd.module import SwinTransformerBlock
+        for key in ("nystrom", "exact"):
+            if key == "exact" and (args.no_exact or w == side):
+                continue
+            torch.manual_seed(7)
+            blk = SwinTransformerBlock(C, heads, w, shift, m=m, attention=key, dtype=tdt)
+            with torch.no_grad():
+                blk.attn.w_qkv.copy_(wq.view(C, 3 * C))
+                blk.attn.b_qkv.copy_(bq)
+                blk.attn.w_proj.copy_(wp.view(C, C))
+                blk.attn.b_proj.copy_(bp)
+            res[f"transformer_block_{key}_us"] = round(timed(lambda: blk(x), reps), 2)
+            del blk
+        if "transformer_block_exact_us" in res:
+            res["transformer_block_speedup_vs_exact"] = round(
+                res["transformer_block_exact_us"] / res["transformer_block_nystrom_us"], 3)
         proj_us = res["block_nystrom_us"] - res["attention_nystrom_us"]
         flops = 8.0 * side * side * C * C   # 2 rows C 3C + 2 rows C C
         res["projections_us"] = round(proj_us, 2)
