@@ -57,8 +57,8 @@ typedef enum { NYSTRA_LM_POOL2D = 0, NYSTRA_LM_SEGMENT1D = 1 } nystra_landmark_m
 
 /* Kernel family.  AUTO picks, for nystra_attn_forward_ex, the MFMA-tiled
  * kernel when the shape is one it covers and the pointers are aligned as it
- * needs (V and O to 16 bytes; for bf16 also Q and K to 4 bytes), and the
- * generic kernel otherwise; nystra_attn_forward_ws may in addition pick the
+ * needs (for bf16, Q, K, V and O to 4 bytes; fp32 needs nothing beyond the
+ * element size), and the generic kernel otherwise; nystra_attn_forward_ws may in addition pick the
  * token-split kernels (see there).  The other values force one
  * (NYSTRA_ERR_UNSUPPORTED if it cannot run this shape, or -- for SPLIT -- if
  * the entry point takes no workspace). */
@@ -208,7 +208,7 @@ int nystra_landmark_pool(const void *Q, const void *K, float *Qbar, float *Kbar,
 int nystra_landmark_map(int N, int m, int mode, int32_t *map_host);
 
 /* Host-only: which kernel family nystra_attn_forward_ex would launch for
- * this shape and options with 16-byte aligned tensors (NYSTRA_VARIANT_GENERIC
+ * this shape and options with aligned tensors (NYSTRA_VARIANT_GENERIC
  * or NYSTRA_VARIANT_TILED), or a negative nystra_status if the arguments are
  * invalid (NYSTRA_VARIANT_SPLIT, which needs a workspace, gives
  * -NYSTRA_ERR_UNSUPPORTED). */

@@ -24,19 +24,14 @@ namespace {
 using namespace tile;
 
 constexpr int kWavesPerBlock = 4;
-typedef __attribute__((address_space(1))) void global_void;
-typedef __attribute__((address_space(3))) void lds_void;
 
-// LDS of one wave: the landmark rows of Q and K (slot layout), a stage that
-// holds V (row-major, as in memory), then the transpose scratch of the
-// pseudo-inverse, then O before its contiguous store, and a row vector.
+// LDS of one wave: the landmark rows of Q and K (slot layout), the transpose
+// scratch of the pseudo-inverse and a row vector (6 KB: V and O move between
+// registers and HBM directly, which leaves room for five waves per SIMD).
 template <class E, int NT, int D>
 struct SmallLds {
-    static constexpr int kBlockFloats = 16 * NT * D * E::bytes / 4;   // one unit's V or O
-    static constexpr int kStage =
-        ((kBlockFloats > 16 * kTrStride ? kBlockFloats : 16 * kTrStride) + 3) / 4 * 4;
+    static constexpr int kStage = 16 * kTrStride;
     static constexpr int kPerWave = 2 * 16 * kLdStride + kStage + 64;
-    static constexpr int kPieces = 16 * NT * D * E::bytes / 16;       // 16-byte pieces of V or O
 };
 
 struct SmallArgs {
@@ -135,9 +130,8 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     const int m = a.m;
     float *qbar = lds_all + wave * L::kPerWave;
     float *kbar = qbar + 16 * kLdStride;
-    float *stage = kbar + 16 * kLdStride;
-    float *scr = stage;   // transpose scratch once V has been read
-    float *vec = stage + L::kStage;
+    float *scr = kbar + 16 * kLdStride;   // transpose scratch
+    float *vec = scr + L::kStage;
 
     const int64_t base = unit * int64_t(N) * D;
     const typename E::T *qu = q + base, *ku = k + base, *vu = v + base;
@@ -158,16 +152,6 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             load_row8<D>(qu + off, qr[tt]);
             load_row8<D>(ku + off, kr[tt]);
         }
-    }
-    // V: the unit's contiguous block, copied to the stage by 16-byte direct
-    // loads (lane l of a round writes piece l of that round).
-    {
-        const char *vb = reinterpret_cast<const char *>(vu);
-#pragma unroll
-        for (int p0 = 0; p0 < L::kPieces; p0 += 64)
-            if (p0 + 64 <= L::kPieces || p0 + lane < L::kPieces)
-                __builtin_amdgcn_global_load_lds((global_void *)(vb + 16 * (p0 + lane)),
-                                                 (lds_void *)(stage + 4 * p0), 16, 0, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
 
@@ -241,11 +225,10 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     if constexpr (!PAD)
         tden = sum_groups(tden);
 
-    // V in the right-hand operand layout of T = G_U^n V: vr[tt][ct][s] =
-    // V[token 16tt+4g+s][feature 16ct+c].  Columns past D read column D-1 and
-    // never reach a stored output; column D becomes the ones column.
-    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): the stage holds V
-    wave_sync();
+    // V in the right-hand operand layout of T = G_U^n V, loaded from HBM:
+    // vr[tt][ct][s] = V[token 16tt+4g+s][feature 16ct+c].  Columns past D read
+    // column D-1 and never reach a stored output; column D becomes the ones
+    // column.
     float vr[NT][NCT][4];
     uint16_t vh[NT][NCT][4];
 #pragma unroll
@@ -259,15 +242,14 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                 const int idx = vlane + (16 * tt + s) * D;
                 const bool ones = PAD && ct == NCT - 1 && f == D;
                 if constexpr (BFM) {
-                    const uint16_t x = reinterpret_cast<const uint16_t *>(stage)[idx];
+                    const uint16_t x = reinterpret_cast<const uint16_t *>(vu)[idx];
                     vh[tt][ct][s] = ones ? uint16_t(0x3F80) : x;   // bf16 1.0
                 } else {
-                    const float x = stage[idx];
+                    const float x = E::load(vu, idx);
                     vr[tt][ct][s] = ones ? 1.f : x;
                 }
             }
     }
-    wave_sync();   // the stage is free again (transpose scratch, then O)
 
     // ---- Step 6, first product: T = G_U^n [V | 1]  (16 landmarks x 16 NCT).
     // T[ct] lane (g,c): T[landmark 4g+i][column 16ct+c].
@@ -444,7 +426,7 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 #pragma unroll
             for (int i = 0; i < 4; ++i)
                 x[i] = on[ct][i] * rcp[i];
-            // O goes to the stage row-major (as in memory).
+            // O straight to HBM, row-major.
             if constexpr (BFM) {
                 // Lanes c and c^1 trade halves: the even lane writes rows 0 and
                 // 2 of features (c, c+1), the odd lane rows 1 and 3 of (c-1, c).
@@ -456,7 +438,7 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                 const uint32_t p1 = odd ? pack_bf16x2(nb[3], x[3]) : pack_bf16x2(x[2], nb[2]);
                 const int fe = 16 * ct + (c & ~1);
                 if (fe < D) {
-                    uint16_t *dst = reinterpret_cast<uint16_t *>(stage) + (4 * g + int(odd)) * D + fe;
+                    uint16_t *dst = reinterpret_cast<uint16_t *>(ou) + (4 * g + int(odd)) * D + fe;
                     *reinterpret_cast<uint32_t *>(dst + 16 * tt * D) = p0;
                     *reinterpret_cast<uint32_t *>(dst + (16 * tt + 2) * D) = p1;
                 }
@@ -464,21 +446,9 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                 if (16 * ct + c < D) {
 #pragma unroll
                     for (int i = 0; i < 4; ++i)
-                        stage[olane + (16 * tt + i) * D + 16 * ct] = x[i];
+                        ou[olane + (16 * tt + i) * D + 16 * ct] = x[i];
                 }
             }
-        }
-    }
-    // ---- Step 7 store: the unit's O block in 16-byte pieces.
-    wave_sync();
-    {
-        char *ob = reinterpret_cast<char *>(ou);
-        const f4 *src = reinterpret_cast<const f4 *>(stage);
-#pragma unroll
-        for (int p0 = 0; p0 < L::kPieces; p0 += 64) {
-            const int p = p0 + lane;
-            if (p0 + 64 <= L::kPieces || p < L::kPieces)
-                *reinterpret_cast<f4 *>(ob + 16 * p) = src[p];
         }
     }
 }
@@ -534,11 +504,9 @@ bool small_supported(const Problem &p)
         return false;
     if (!is_pow2(g.cols) || !is_pow2(g.pr) || !is_pow2(g.pc) || !is_pow2(g.gc))
         return false;
-    // V and O move as whole 16-byte pieces; bf16 row chunks of Q and K are
-    // read as 16-byte pieces that start at even elements.
-    if ((uintptr_t(p.v) | uintptr_t(p.o)) % 16 != 0)
-        return false;
-    if (p.dtype == 1 && (uintptr_t(p.q) | uintptr_t(p.k)) % 4 != 0)
+    // bf16 row chunks of Q and K are read as 16-byte pieces that start at even
+    // elements, and O is written in pairs of features.
+    if (p.dtype == 1 && (uintptr_t(p.q) | uintptr_t(p.k) | uintptr_t(p.o)) % 4 != 0)
         return false;
     return true;
 }

@@ -390,9 +390,9 @@ def test_output_untouched_on_validation_error():
     assert bool((o == 7.0).all())
 
 
-# (dtype, element offset, does a tiled kernel take it): fp32 at 4 bytes runs the
-# multi-wave tiled kernel (the 64-token one needs V and O 16-byte aligned), bf16
-# at 2 bytes has no tiled kernel, 16-byte offsets run the 64-token kernel.
+# (dtype, element offset, does a tiled kernel take it): fp32 tiled kernels take
+# any element alignment; bf16 needs 4-byte aligned tensors (2 bytes: the generic
+# kernel runs).
 ALIGN = [("f32", 1, True), ("bf16", 1, False), ("f32", 4, True), ("bf16", 8, True)]
 
 
