@@ -127,7 +127,7 @@ int nystra_attn_forward_ex(const void *Q, const void *K, const void *V, void *O,
  * nystra_attn_workspace_size stores in *bytes the device workspace that
  * nystra_attn_forward_ws needs for these arguments: 0 unless the call would
  * run the token-split kernels.  AUTO chooses them when the shape is supported
- * (N % 16 == 0, d_h in {8, 16, 24, 30, 32}, m <= 64; for bf16, Q, K, V 4-byte
+ * (N % 16 == 0, d_h a multiple of 4 in 8..32 or 30, m <= 64; for bf16, Q, K, V 4-byte
  * aligned; O 16-byte aligned) and N >= 4096, or N >= 2048 with fewer than 512
  * units; NYSTRA_VARIANT_SPLIT forces them.  The size depends on the arguments
  * only, not on any pointer (aligned tensors are assumed), and is about

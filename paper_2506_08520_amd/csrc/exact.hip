@@ -263,8 +263,11 @@ void launch_exact_tiled_e(const Problem &p, hipStream_t stream)
 {
     switch (p.d) {
     case 8: launch_exact_tiled<E, 8>(p, stream); break;
+    case 12: launch_exact_tiled<E, 12>(p, stream); break;
     case 16: launch_exact_tiled<E, 16>(p, stream); break;
+    case 20: launch_exact_tiled<E, 20>(p, stream); break;
     case 24: launch_exact_tiled<E, 24>(p, stream); break;
+    case 28: launch_exact_tiled<E, 28>(p, stream); break;
     case 30: launch_exact_tiled<E, 30>(p, stream); break;
     default: launch_exact_tiled<E, 32>(p, stream); break;
     }

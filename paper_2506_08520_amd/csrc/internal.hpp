@@ -66,7 +66,8 @@ struct BlockGemm {
 bool block_gemm_supported(int64_t rows, int C);
 hipError_t launch_block_gemm(const BlockGemm &g, hipStream_t stream);
 
-// Head widths with a tiled instantiation.
-inline bool tiled_width(int d) { return d == 8 || d == 16 || d == 24 || d == 30 || d == 32; }
+// Head widths with a tiled instantiation: the multiples of 4 from 8 to 32
+// (Dehazeformer's 12 and 16, Uformer's 32) and SwinIR's 30.
+inline bool tiled_width(int d) { return d >= 8 && d <= 32 && (d % 4 == 0 || d == 30); }
 
 }  // namespace nystra

@@ -775,8 +775,11 @@ void launch_split_e(const Problem &p, const Plan &s, const SplitArgs &a, hipStre
 {
     switch (p.d) {
     case 8: launch_split_d<E, 8>(p, s, a, stream); break;
+    case 12: launch_split_d<E, 12>(p, s, a, stream); break;
     case 16: launch_split_d<E, 16>(p, s, a, stream); break;
+    case 20: launch_split_d<E, 20>(p, s, a, stream); break;
     case 24: launch_split_d<E, 24>(p, s, a, stream); break;
+    case 28: launch_split_d<E, 28>(p, s, a, stream); break;
     case 30: launch_split_d<E, 30>(p, s, a, stream); break;
     default: launch_split_d<E, 32>(p, s, a, stream); break;
     }

@@ -1,5 +1,5 @@
 // MFMA-tiled PnP-Nystra kernel for small windows (N = 16, 32 or 64 tokens,
-// m <= 16 landmarks, d_h in {8, 16, 24, 30, 32}): one wavefront computes one
+// m <= 16 landmarks, d_h in {8, 12, ..., 28, 30, 32}): one wavefront computes one
 // (window, head) unit entirely in registers (register tiles in the D-layout of
 // tile_common.hpp), with LDS used only for a few small exchanges.  fp32 inputs
 // run every contraction on v_mfma_f32_16x16x4f32; bf16 inputs run the
@@ -490,8 +490,11 @@ void launch_small_e(const Problem &p, const SmallArgs &a, hipStream_t stream)
 {
     switch (p.d) {
     case 8: launch_small_d<E, 8>(p, a, stream); break;
+    case 12: launch_small_d<E, 12>(p, a, stream); break;
     case 16: launch_small_d<E, 16>(p, a, stream); break;
+    case 20: launch_small_d<E, 20>(p, a, stream); break;
     case 24: launch_small_d<E, 24>(p, a, stream); break;
+    case 28: launch_small_d<E, 28>(p, a, stream); break;
     case 30: launch_small_d<E, 30>(p, a, stream); break;
     default: launch_small_d<E, 32>(p, a, stream); break;
     }

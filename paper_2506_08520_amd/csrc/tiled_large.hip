@@ -1,5 +1,5 @@
 // MFMA-tiled PnP-Nystra kernel for large windows (N a multiple of 16, e.g.
-// 16x16 and 32x32 windows; m <= 64 landmarks; d_h in {8, 16, 24, 30, 32}).
+// 16x16 and 32x32 windows; m <= 64 landmarks; d_h in {8, 12, ..., 28, 30, 32}).
 //
 // One workgroup computes one (window, head) unit with MT = ceil(m / 16)
 // wavefronts; wave w owns landmark tile w (landmarks 16w .. 16w+15):
@@ -393,8 +393,11 @@ void launch_large_e(const Problem &p, const LargeArgs &a, hipStream_t stream)
 {
     switch (p.d) {
     case 8: launch_large_m<E, 8>(p, a, stream); break;
+    case 12: launch_large_m<E, 12>(p, a, stream); break;
     case 16: launch_large_m<E, 16>(p, a, stream); break;
+    case 20: launch_large_m<E, 20>(p, a, stream); break;
     case 24: launch_large_m<E, 24>(p, a, stream); break;
+    case 28: launch_large_m<E, 28>(p, a, stream); break;
     case 30: launch_large_m<E, 30>(p, a, stream); break;
     default: launch_large_m<E, 32>(p, a, stream); break;
     }

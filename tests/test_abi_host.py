@@ -158,6 +158,11 @@ def test_status_strings_and_opts(L):
 
 
 def test_variant_selection():
+    # tiled head widths: multiples of 4 from 8 to 32, and 30
+    for d in range(1, 65):
+        tiled = 8 <= d <= 32 and (d % 4 == 0 or d == 30)
+        sel = B.nystra_select_variant(256, d, 16)
+        assert sel == (B.VARIANT_TILED if tiled else B.VARIANT_GENERIC), d
     g = B.VARIANT_GENERIC
     assert B.nystra_select_variant(64, 30, 16, opts=B.make_opts(variant=g)) == g
     assert B.nystra_select_variant(49, 64, 7) in (B.VARIANT_GENERIC, B.VARIANT_TILED)
@@ -190,7 +195,7 @@ def test_workspace_size():
     assert ws_size(1, 2, 1 << 16, 32, 64) < ws_size(1, 2, 1 << 18, 32, 64)
     assert ws_size(0, 6, 1 << 18, 32, 64) == 0
     # shapes the token-split kernels do not cover
-    for args in [(1, 1, 16384, 20, 64), (1, 1, 100, 32, 4), (1, 1, 16384, 48, 64)]:
+    for args in [(1, 1, 16384, 22, 64), (1, 1, 100, 32, 4), (1, 1, 16384, 48, 64)]:
         with pytest.raises(B.NystraError) as e:
             ws_size(*args, variant=split)
         assert e.value.status == EUNSUP

@@ -44,7 +44,8 @@ CASES = [
     # that fp32-sized input noise moves the float64 oracle by 4e-5 at outputs
     # of 19; m = 8 is not.)
     (1, 12, 20, 24, 3, 4, 2, 8, "f32", "nystrom"),
-    (1, 16, 16, 60, 3, 8, 3, 16, "f32", "nystrom"),     # d_h = 20: generic attention kernel
+    (1, 16, 16, 66, 3, 8, 3, 16, "f32", "nystrom"),     # d_h = 22: generic attention kernel
+    (1, 32, 32, 24, 2, 8, 4, 16, "bf16", "nystrom"),    # Dehazeformer-shaped: d_h = 12
     (2, 16, 16, 96, 3, 8, 4, 0, "f32", "exact"),
     (1, 16, 16, 180, 6, 16, 8, 0, "bf16", "exact"),
     (1, 64, 64, 64, 2, 64, 0, 64, "f32", "nystrom"),    # one window per map: token-split path
