@@ -107,16 +107,34 @@ __device__ inline SplitTile split_tile(f4 x)
     return SplitTile{__builtin_bit_cast(bf8, u)};
 }
 
-// L * R for 16x16 tiles given LT = L^T and R in split form: the two
-// products (L_hi + L_lo) R_hi and (L_hi + L_lo) R_lo on the bf16 matrix
-// cores, accumulated in fp32.
-__device__ inline f4 mm16_split(const SplitTile &LT, const SplitTile &R)
+// A split tile in both orders of its k slots: hl = [hi | lo] (the packing of
+// SplitTile) and lh = [lo | hi].
+struct SplitPair {
+    bf8 hl, lh;
+};
+
+__device__ inline SplitPair both_orders(bf8 hl)
 {
-    const U16B r = __builtin_bit_cast(U16B, R.hl);
-    const U16B rh = {{r.w[0], r.w[1], r.w[0], r.w[1]}};
-    const U16B rl = {{r.w[2], r.w[3], r.w[2], r.w[3]}};
-    const f4 acc = mfma_bf16(LT.hl, __builtin_bit_cast(bf8, rh), f4{0.f, 0.f, 0.f, 0.f});
-    return mfma_bf16(LT.hl, __builtin_bit_cast(bf8, rl), acc);
+    const U16B u = __builtin_bit_cast(U16B, hl);
+    const U16B v = {{u.w[2], u.w[3], u.w[0], u.w[1]}};
+    return SplitPair{hl, __builtin_bit_cast(bf8, v)};
+}
+
+// L * R for 16x16 tiles with both factors split into bf16 hi + lo terms, on
+// the bf16 matrix cores with fp32 accumulation.  Pairing [hi | lo] with
+// [hi | lo] gives L_hi R_hi + L_lo R_lo; pairing [lo | hi] with [hi | lo]
+// gives the two cross terms; together the full product of the two sums.
+// mm16_hl takes LT = L^T in both orders, mm16_lh R in both orders.
+__device__ inline f4 mm16_hl(const SplitPair &LT, bf8 R)
+{
+    const f4 acc = mfma_bf16(LT.hl, R, f4{0.f, 0.f, 0.f, 0.f});
+    return mfma_bf16(LT.lh, R, acc);
+}
+
+__device__ inline f4 mm16_lh(bf8 LT, const SplitPair &R)
+{
+    const f4 acc = mfma_bf16(LT, R.hl, f4{0.f, 0.f, 0.f, 0.f});
+    return mfma_bf16(LT, R.lh, acc);
 }
 
 // Orders the LDS traffic of one wavefront (all lanes execute in lockstep, so
@@ -138,6 +156,33 @@ __device__ inline f4 transpose16(f4 M, float *scr, int g, int c)
     f4 r = *reinterpret_cast<const f4 *>(scr + c * kTrStride + 4 * g);
     wave_sync();
     return r;
+}
+
+// Transpose of a split D-layout tile through the wave's LDS scratch (at least
+// 16 * kTrStride floats): the bf16 terms move as 16-bit values, so the split
+// of M^T costs no arithmetic.  Element (r, col) of plane p (0 = hi, 1 = lo)
+// sits at bf16 index r * 40 + (col / 4) * 8 + 4p + col % 4, so that a lane
+// reads its [hi | lo] chunk of a transposed row with one 16-byte load.
+__device__ inline SplitPair transpose_split(bf8 s, float *scr, int g, int c)
+{
+    static_assert(16 * 40 * 2 <= 16 * kTrStride * 4, "scratch holds both planes");
+    uint16_t *b = reinterpret_cast<uint16_t *>(scr);
+    const U16B u = __builtin_bit_cast(U16B, s);
+    const int col = (c >> 2) * 8 + (c & 3);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int at = (4 * g + i) * 40 + col;
+        b[at] = uint16_t(u.w[i >> 1] >> (16 * (i & 1)));
+        b[at + 4] = uint16_t(u.w[2 + (i >> 1)] >> (16 * (i & 1)));
+    }
+    wave_sync();
+    const uint16_t *row = b + c * 40 + 8 * g;
+    const U16B hl = *reinterpret_cast<const U16B *>(row);
+    typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+    const u2 h = *reinterpret_cast<const u2 *>(row), l = *reinterpret_cast<const u2 *>(row + 4);
+    wave_sync();
+    const U16B lh = {{l[0], l[1], h[0], h[1]}};
+    return SplitPair{__builtin_bit_cast(bf8, hl), __builtin_bit_cast(bf8, lh)};
 }
 
 // Per-token vector exchange: value x (held per lane column c, identical in

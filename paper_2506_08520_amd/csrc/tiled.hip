@@ -42,6 +42,33 @@ struct SmallArgs {
     int lg_cols, lg_pr, lg_pc, lg_gc, free_bits;   // pooling grid (log2 sizes)
 };
 
+// Pooling grids of the 8x8 windows that restoration models use, fixed at
+// compile time so that the patch-sum exchanges need no uniform branches:
+// kGrid2x2 is m = 16 (4 x 4 patches of 2 x 2 tokens), kGrid2x4 is m = 8
+// (4 x 2 patches of 2 rows x 4 columns).  kGridAny reads the grid from
+// SmallArgs.  The arithmetic is the same either way, so the outputs are
+// identical bit for bit.
+enum { kGridAny = 0, kGrid2x2 = 1, kGrid2x4 = 2 };
+
+template <int GRID>
+__device__ inline void fix_grid(SmallArgs &a)
+{
+    if constexpr (GRID == kGrid2x2) {
+        a.lg_cols = 3; a.lg_pr = 1; a.lg_pc = 1; a.lg_gc = 2; a.free_bits = 1 | 8;
+    } else if constexpr (GRID == kGrid2x4) {
+        a.lg_cols = 3; a.lg_pr = 1; a.lg_pc = 2; a.lg_gc = 1; a.free_bits = 3 | 8;
+    }
+}
+
+int grid_of(const SmallArgs &a, int N)
+{
+    if (N == 64 && a.lg_cols == 3 && a.lg_pr == 1 && a.lg_pc == 1 && a.lg_gc == 2 && a.free_bits == 9)
+        return kGrid2x2;
+    if (N == 64 && a.lg_cols == 3 && a.lg_pr == 1 && a.lg_pc == 2 && a.lg_gc == 1 && a.free_bits == 11)
+        return kGrid2x4;
+    return kGridAny;
+}
+
 // Step 1 for one input: the patch sums of this wave's tokens (the mean times
 // the patch size; the factor is folded into the logit scales, exactly, since
 // the patch size is a power of two), written to bar[l][8g + s] in the slot
@@ -107,12 +134,13 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi)
     return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2{lo, hi}), b2));   // RNE
 }
 
-template <class E, int NT, int D, bool BFM>
+template <class E, int NT, int D, bool BFM, int GRID>
 __global__ void __launch_bounds__(64 * kWavesPerBlock)
 tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__restrict__ k,
                    const typename E::T *__restrict__ v, typename E::T *__restrict__ o,
                    SmallArgs a)
 {
+    fix_grid<GRID>(a);
     constexpr int N = 16 * NT;
     constexpr int NCT = (D + 15) / 16;   // 16-wide feature tiles of V, T, W and O
     // With a spare feature column (D not a multiple of 16), column D of V is
@@ -347,26 +375,42 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 #pragma unroll
     for (int i = 0; i < 4; ++i)
         eye[i] = (4 * g + i == c && c < m) ? 1.f : 0.f;
+    // The factor 1/4 of the update rides on A: with X' = (A/4) Z = X/4,
+    //   4 Y1 = 28I - 16X',  Y2 = 15I - X' (4 Y1),  Y3 / 4 = 13I/4 - X' Y2,
+    // and Z <- Z (Y3 / 4).  Scaling by powers of two is exact, so every value
+    // equals the one of the update as written.
+    const f4 ATq = AT * 0.25f, e28 = eye * 28.f, e15 = eye * 15.f, e13q = eye * 3.25f;
     if constexpr (BFM) {
-        // bf16 inputs: every product as (hi + lo) x (hi + lo) bf16 terms.
-        const SplitTile ATs = split_tile(AT);
+        // bf16 inputs: every product as (hi + lo) x (hi + lo) bf16 terms; the
+        // left factors come in both k orders, X'^T and Z^T by moving the split
+        // terms of X' and Z through LDS.
+        const SplitPair Aq = both_orders(split_tile(ATq).hl);
         for (int it = 0; it < a.iters; ++it) {
-            const f4 X = mm16_split(ATs, split_tile(Z));
-            const SplitTile XTs = split_tile(transpose16(X, scr, g, c));
-            f4 Y = eye * 7.f - X;
-            Y = eye * 15.f - mm16_split(XTs, split_tile(Y));
-            Y = eye * 13.f - mm16_split(XTs, split_tile(Y));
-            Z = mm16_split(split_tile(ZT), split_tile(Y)) * 0.25f;
-            ZT = transpose16(Z, scr, g, c);
+            const bf8 zs = split_tile(Z).hl;
+            const SplitPair ZTs = transpose_split(zs, scr, g, c);
+            const f4 Xq = mm16_hl(Aq, zs);
+            const SplitPair XTq = transpose_split(split_tile(Xq).hl, scr, g, c);
+            f4 Y;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                Y[i] = fmaf(Xq[i], -16.f, e28[i]);
+            Y = e15 - mm16_hl(XTq, split_tile(Y).hl);
+            Y = e13q - mm16_hl(XTq, split_tile(Y).hl);
+            Z = mm16_hl(ZTs, split_tile(Y).hl);
         }
+        if (a.iters > 0)
+            ZT = transpose16(Z, scr, g, c);
     } else {
         for (int it = 0; it < a.iters; ++it) {
-            const f4 X = mm16(AT, Z);
-            const f4 XT = transpose16(X, scr, g, c);
-            f4 Y = eye * 7.f - X;
-            Y = eye * 15.f - mm16(XT, Y);
-            Y = eye * 13.f - mm16(XT, Y);
-            Z = mm16(ZT, Y) * 0.25f;
+            const f4 Xq = mm16(ATq, Z);
+            const f4 XTq = transpose16(Xq, scr, g, c);
+            f4 Y;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                Y[i] = fmaf(Xq[i], -16.f, e28[i]);
+            Y = e15 - mm16(XTq, Y);
+            Y = e13q - mm16(XTq, Y);
+            Z = mm16(ZT, Y);
             ZT = transpose16(Z, scr, g, c);
         }
     }
@@ -383,12 +427,12 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             sum_groups(ZT[0] * td[0] + ZT[1] * td[1] + ZT[2] * td[2] + ZT[3] * td[3]);
         wd = by_rows(wden, vec, g, c);
     }
-    // bf16 path: W as hi + lo terms.
-    SplitTile ws[NCT];
+    // bf16 path: W as hi + lo terms, in both k orders.
+    SplitPair ws[NCT];
     if constexpr (BFM) {
 #pragma unroll
         for (int ct = 0; ct < NCT; ++ct)
-            ws[ct] = split_tile(Wt[ct]);
+            ws[ct] = both_orders(split_tile(Wt[ct]).hl);
     }
 
     // ---- Steps 3 (G_L side), 6 and 7 per token tile: O = G_L^n W / O_D.
@@ -397,13 +441,13 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt) {
         f4 on[NCT];
-        SplitTile gs;
+        bf8 gs;
         if constexpr (BFM)
-            gs = split_tile(glT[tt]);
+            gs = split_tile(glT[tt]).hl;
 #pragma unroll
         for (int ct = 0; ct < NCT; ++ct) {
             if constexpr (BFM)
-                on[ct] = mm16_split(gs, ws[ct]);   // (G_hi + G_lo)(W_hi + W_lo)
+                on[ct] = mm16_lh(gs, ws[ct]);   // (G_hi + G_lo)(W_hi + W_lo)
             else
                 on[ct] = mm16(glT[tt], Wt[ct]);
         }
@@ -463,11 +507,11 @@ int ilog2(int x)
     return r;
 }
 
-template <class E, int NT, int D>
+template <class E, int NT, int D, int GRID = kGridAny>
 void launch_small(const Problem &p, const SmallArgs &a, hipStream_t stream)
 {
     const unsigned blocks = unsigned((p.units + kWavesPerBlock - 1) / kWavesPerBlock);
-    hipLaunchKernelGGL((tiled_small_kernel<E, NT, D, E::bytes == 2>), dim3(blocks),
+    hipLaunchKernelGGL((tiled_small_kernel<E, NT, D, E::bytes == 2, GRID>), dim3(blocks),
                        dim3(64 * kWavesPerBlock),
                        0, stream, static_cast<const typename E::T *>(p.q),
                        static_cast<const typename E::T *>(p.k),
@@ -481,7 +525,13 @@ void launch_small_d(const Problem &p, const SmallArgs &a, hipStream_t stream)
     switch (p.N) {
     case 16: launch_small<E, 1, D>(p, a, stream); break;
     case 32: launch_small<E, 2, D>(p, a, stream); break;
-    default: launch_small<E, 4, D>(p, a, stream); break;
+    default:
+        switch (grid_of(a, p.N)) {
+        case kGrid2x2: launch_small<E, 4, D, kGrid2x2>(p, a, stream); break;
+        case kGrid2x4: launch_small<E, 4, D, kGrid2x4>(p, a, stream); break;
+        default: launch_small<E, 4, D>(p, a, stream); break;
+        }
+        break;
     }
 }
 
