@@ -198,8 +198,9 @@ __device__ inline f4 by_rows(float x, float *vec, int g, int c)
 }
 
 // ---- cross-lane operations (wave64; a "row" is 16 lanes) ------------------
-// DPP forms fuse into the consuming VALU instruction; swizzle and bpermute
-// go through the LDS crossbar without touching LDS memory.
+// DPP forms fuse into the consuming VALU instruction and the permlane swaps
+// are VALU instructions; the swizzle goes through the LDS crossbar without
+// touching LDS memory.
 
 __device__ inline float dpp_xor1(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0xB1, 0xF, 0xF, false); }
 __device__ inline float dpp_xor2(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0x4E, 0xF, 0xF, false); }
@@ -209,44 +210,54 @@ __device__ inline float dpp_ror4(float x) { return __builtin_amdgcn_update_dpp(0
 // Rotating a 16-lane row by 8 is the exchange of lanes c and c ^ 8.
 __device__ inline float dpp_xor8(float x) { return __builtin_amdgcn_update_dpp(0.f, x, 0x128, 0xF, 0xF, true); }
 
-// Value of lane (lane & 16) | src within each 32-lane half: with src < 16,
-// every lane of a 16-lane row receives the value of that row's lane src.
+// Every lane of a 16-lane row receives the value of that row's lane SRC
+// (DPP row_newbcast, a VALU operand modifier).
 template <int SRC>
 __device__ inline float row_bcast(float x)
 {
     static_assert(SRC >= 0 && SRC < 16, "source lane within the row");
-    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x),
-                                                                 0x10 | (SRC << 5)));
+    return __builtin_amdgcn_update_dpp(0.f, x, 0x150 + SRC, 0xF, 0xF, true);
 }
 __device__ inline float swz_xor4(float x)
 {
     return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x101F));
 }
 
-// Exchange with lane ^ 16 (swizzle inside each 32-lane half) and with
-// lane ^ 32 (permute through the LDS crossbar; no LDS memory is used).
-__device__ inline float swz_xor16(float x)
+// Pairs (x[l], x[l ^ 16]) and (x[l], x[l ^ 32]) in VALU registers: the
+// permlane swaps of a value with itself leave, in every lane, the row (half)
+// of the pair with the lower index in .first and the other in .second.
+struct LanePair {
+    float first, second;
+};
+
+__device__ inline LanePair pair_xor16(float x)
 {
-    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x401F));
+    const auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(unsigned, x),
+                                                    __builtin_bit_cast(unsigned, x), false, false);
+    return LanePair{__builtin_bit_cast(float, unsigned(r[0])), __builtin_bit_cast(float, unsigned(r[1]))};
 }
 
-__device__ inline float perm_xor32(float x)
+__device__ inline LanePair pair_xor32(float x)
 {
-    const int addr = int((__lane_id() ^ 32u) << 2);
-    return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(addr, __builtin_bit_cast(int, x)));
+    const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x),
+                                                    __builtin_bit_cast(unsigned, x), false, false);
+    return LanePair{__builtin_bit_cast(float, unsigned(r[0])), __builtin_bit_cast(float, unsigned(r[1]))};
 }
 
-// Sum / max over the four lanes c, c^16, c^32, c^48 (the lane groups g).
+// Sum / max over the four lanes c, c^16, c^32, c^48 (the lane groups g);
+// every lane gets the same bits.
 __device__ inline float sum_groups(float x)
 {
-    x += swz_xor16(x);
-    return x + perm_xor32(x);
+    const LanePair a = pair_xor16(x);
+    const LanePair b = pair_xor32(a.first + a.second);
+    return b.first + b.second;
 }
 
 __device__ inline float max_groups(float x)
 {
-    x = fmaxf(x, swz_xor16(x));
-    return fmaxf(x, perm_xor32(x));
+    const LanePair a = pair_xor16(x);
+    const LanePair b = pair_xor32(fmaxf(a.first, a.second));
+    return fmaxf(b.first, b.second);
 }
 
 // Sum / max over the 16 lanes of a row.
