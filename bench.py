@@ -24,13 +24,17 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E peak, GB/s
 ROTATE_BYTES = 1.2 * (1 << 30)  # working set cycled by the timed steps
+WARMUP_SECONDS = 1.0           # default warm-up: long enough for steady clocks
 
 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed launches before the timed ones (default: as many as run "
+                         "in about one second, so the GPU reaches its steady clocks; the "
+                         "count used is reported)")
     ap.add_argument("--config", default="c2")
     ap.add_argument("--dtype", default="f32", choices=["f32", "bf16"])
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -83,8 +87,19 @@ def time_kernel(case, launch, steps, warmup):
     kernels are launched on."""
     import torch
     stream = torch.cuda.current_stream()
-    for i in range(warmup):
-        launch(*case.sets[i % case.nsets], stream)
+    if warmup is None:
+        # Warm up for about one second (checked every 64 launches).
+        warmup, t_end = 0, time.perf_counter() + WARMUP_SECONDS
+        while True:
+            for _ in range(64):
+                launch(*case.sets[warmup % case.nsets], stream)
+                warmup += 1
+            torch.cuda.synchronize()
+            if time.perf_counter() >= t_end:
+                break
+    else:
+        for i in range(warmup):
+            launch(*case.sets[i % case.nsets], stream)
     r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -104,7 +119,7 @@ def time_kernel(case, launch, steps, warmup):
         stops[i].record(stream)
     torch.cuda.synchronize()
     pairs = sum(a.elapsed_time(b) for a, b in zip(starts, stops)) / n
-    return (t1 - t0) * 1e3 / steps, region, pairs
+    return (t1 - t0) * 1e3 / steps, region, pairs, warmup
 
 
 def measured_traffic(cfg, dtype, variant):
@@ -382,12 +397,13 @@ def main():
         def ex(q_, k_, v_, o_, s):
             B.nystra_exact_attn_forward(q_, k_, v_, out=o_, stream=s)
 
-        ms, kern, pairs = time_kernel(case, nys, args.steps, args.warmup)
+        ms, kern, pairs, warm = time_kernel(case, nys, args.steps, args.warmup)
         r = {"ms_per_step": ms, "kernel_ms": kern, "pairs_ms": pairs, "io_bytes": case.io_bytes,
+             "warmup": warm,
              "variant": B.nystra_select_variant(wl.N, wl.d, wl.m,
                                                 B.F32 if dt == "f32" else B.BF16)}
         if not args.no_exact:
-            ems, ekern, _ = time_kernel(case, ex, max(10, args.steps // 4), args.warmup)
+            ems, ekern, _, _ = time_kernel(case, ex, max(10, args.steps // 4), args.warmup)
             r.update(exact_ms_per_step=ems, exact_kernel_ms=ekern)
         results[dt] = r
         del case
@@ -403,7 +419,7 @@ def main():
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": args.warmup,
+        "warmup": r["warmup"],
         "ms_per_step": r["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
