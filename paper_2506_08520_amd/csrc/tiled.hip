@@ -187,6 +187,33 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             load_row8<D>(ku + off, kr[tt]);
         }
     }
+    // V in the right-hand operand layout of T = G_U^n V, loaded from HBM
+    // together with Q and K, so that a unit's three blocks arrive together:
+    // vr[tt][ct][s] = V[token 16tt+4g+s][feature 16ct+c].  Columns past D read
+    // column D-1 and never reach a stored output; column D becomes the ones
+    // column.
+    float vr[NT][NCT][4];
+    uint16_t vh[NT][NCT][4];
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) {
+        const int f = 16 * ct + c;
+        const int vlane = 4 * g * D + min(f, D - 1);
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const int idx = vlane + (16 * tt + s) * D;
+                const bool ones = PAD && ct == NCT - 1 && f == D;
+                if constexpr (BFM) {
+                    const uint16_t x = reinterpret_cast<const uint16_t *>(vu)[idx];
+                    vh[tt][ct][s] = ones ? uint16_t(0x3F80) : x;   // bf16 1.0
+                } else {
+                    const float x = E::load(vu, idx);
+                    vr[tt][ct][s] = ones ? 1.f : x;
+                }
+            }
+    }
+
     __builtin_amdgcn_sched_barrier(0);
 
     // Landmark rows m..15 are padding: zero them so they contribute nothing.
@@ -258,32 +285,6 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         }
     if constexpr (!PAD)
         tden = sum_groups(tden);
-
-    // V in the right-hand operand layout of T = G_U^n V, loaded from HBM:
-    // vr[tt][ct][s] = V[token 16tt+4g+s][feature 16ct+c].  Columns past D read
-    // column D-1 and never reach a stored output; column D becomes the ones
-    // column.
-    float vr[NT][NCT][4];
-    uint16_t vh[NT][NCT][4];
-#pragma unroll
-    for (int ct = 0; ct < NCT; ++ct) {
-        const int f = 16 * ct + c;
-        const int vlane = 4 * g * D + min(f, D - 1);
-#pragma unroll
-        for (int tt = 0; tt < NT; ++tt)
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                const int idx = vlane + (16 * tt + s) * D;
-                const bool ones = PAD && ct == NCT - 1 && f == D;
-                if constexpr (BFM) {
-                    const uint16_t x = reinterpret_cast<const uint16_t *>(vu)[idx];
-                    vh[tt][ct][s] = ones ? uint16_t(0x3F80) : x;   // bf16 1.0
-                } else {
-                    const float x = E::load(vu, idx);
-                    vr[tt][ct][s] = ones ? 1.f : x;
-                }
-            }
-    }
 
     // ---- Step 6, first product: T = G_U^n [V | 1]  (16 landmarks x 16 NCT).
     // T[ct] lane (g,c): T[landmark 4g+i][column 16ct+c].
