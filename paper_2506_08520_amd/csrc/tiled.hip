@@ -134,14 +134,18 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi)
     return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2{lo, hi}), b2));   // RNE
 }
 
-// bf16 inputs run at most four waves per SIMD: at the SwinIR-like layer
-// (6144 units, six per SIMD) the first four waves' computation then overlaps
-// the loads of the remaining two, which measured 11% faster than all six
-// resident at once (every load issued at the start, then every computation).
-// fp32 inputs are bound by their matrix work and run at full occupancy.
+// Resident waves per SIMD are capped below what the registers allow (three
+// for fp32, four for bf16): with fewer waves resident than units per SIMD,
+// the waves that start later load their inputs while the first ones
+// compute.  With every unit resident at once (the SwinIR-like layer has six
+// per SIMD) all loads are issued at the start and all computation follows.
+// On that layer the caps measured fastest (fp32 47.2 -> 45.1 us at three
+// waves instead of four, bf16 33.8 -> 29.9 us at four instead of six); on
+// L2-resident inputs the computation alone runs at the same speed from three
+// to six waves.
 template <class E, int NT, int D, bool BFM, int GRID>
 __global__ void __launch_bounds__(64 * kWavesPerBlock)
-__attribute__((amdgpu_waves_per_eu(1, BFM ? 4 : 8)))
+__attribute__((amdgpu_waves_per_eu(1, BFM ? 4 : 3)))
 tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__restrict__ k,
                    const typename E::T *__restrict__ v, typename E::T *__restrict__ o,
                    SmallArgs a)
