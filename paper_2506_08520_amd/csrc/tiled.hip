@@ -25,13 +25,27 @@ using namespace tile;
 
 constexpr int kWavesPerBlock = 4;
 
-// LDS of one wave: the landmark rows of Q and K (slot layout), the transpose
-// scratch of the pseudo-inverse and a row vector (6 KB: V and O move between
-// registers and HBM directly, which leaves room for five waves per SIMD).
-template <class E, int NT, int D>
+// Pooling grids of the 8x8 windows that restoration models use, fixed at
+// compile time: kGrid2x2 is m = 16 (4 x 4 patches of 2 x 2 tokens), kGrid2x4
+// is m = 8 (4 x 2 patches of 2 rows x 4 columns).  kGridAny reads the grid
+// from SmallArgs.
+enum { kGridAny = 0, kGrid2x2 = 1, kGrid2x4 = 2 };
+
+// Row stride (floats) of the raw Q / K chunks staged for the fixed grids: a
+// token's four 8-feature chunks plus 16 bytes of padding.
+template <class E>
+constexpr int raw_stride() { return E::bytes == 4 ? 36 : 20; }
+
+// LDS of one wave: the landmark rows of Q and K (slot layout; with a fixed
+// grid, the staged raw chunks of one input instead), the transpose scratch of
+// the pseudo-inverse and a row vector.  V and O move between registers and
+// HBM directly.
+template <class E, int NT, int D, int GRID>
 struct SmallLds {
+    static constexpr int kRows =
+        GRID == kGridAny ? 2 * 16 * kLdStride : 16 * NT * raw_stride<E>();
     static constexpr int kStage = 16 * kTrStride;
-    static constexpr int kPerWave = 2 * 16 * kLdStride + kStage + 64;
+    static constexpr int kPerWave = kRows + kStage + 64;
 };
 
 struct SmallArgs {
@@ -41,14 +55,6 @@ struct SmallArgs {
     float inv_patch;   // 1 / tokens per pooling patch (a power of two)
     int lg_cols, lg_pr, lg_pc, lg_gc, free_bits;   // pooling grid (log2 sizes)
 };
-
-// Pooling grids of the 8x8 windows that restoration models use, fixed at
-// compile time so that the patch-sum exchanges need no uniform branches:
-// kGrid2x2 is m = 16 (4 x 4 patches of 2 x 2 tokens), kGrid2x4 is m = 8
-// (4 x 2 patches of 2 rows x 4 columns).  kGridAny reads the grid from
-// SmallArgs.  The arithmetic is the same either way, so the outputs are
-// identical bit for bit.
-enum { kGridAny = 0, kGrid2x2 = 1, kGrid2x4 = 2 };
 
 template <int GRID>
 __device__ inline void fix_grid(SmallArgs &a)
@@ -127,6 +133,61 @@ __device__ inline void pool_to_lds(Get get, float *bar, const SmallArgs &a, int 
     }
 }
 
+// Step 1 for a fixed grid, one input: every lane stages its raw chunks (one
+// per token tile) in LDS rows by token, then lane (g, c) adds the chunks of
+// the tokens of landmark c's patch, in patch order: out[s] = patch sum of
+// slot s of group g (zero in overlapping slots and for padding landmarks).
+template <class E, int NT, int D, int GRID, class Chunk>
+__device__ inline void pool_direct(const Chunk (&x)[NT], float *stage, float (&out)[8], int m,
+                                   int g, int c)
+{
+    constexpr int RS = raw_stride<E>();
+    constexpr int PR = 2, PC = GRID == kGrid2x2 ? 2 : 4, GC = 8 / PC;   // 8 x 8 window
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt) {
+        float *row = stage + (16 * tt + c) * RS + (E::bytes == 4 ? 8 : 4) * g;
+        if constexpr (E::bytes == 4) {
+            reinterpret_cast<f4 *>(row)[0] = f4{x[tt][0], x[tt][1], x[tt][2], x[tt][3]};
+            reinterpret_cast<f4 *>(row)[1] = f4{x[tt][4], x[tt][5], x[tt][6], x[tt][7]};
+        } else {
+            *reinterpret_cast<U16B *>(row) = __builtin_bit_cast(U16B, x[tt]);
+        }
+    }
+    wave_sync();
+    const int le = min(c, m - 1);   // padding lanes read a valid patch, then drop it
+    const int r0 = (le / GC) * PR, c0 = (le % GC) * PC;
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+        out[s] = 0.f;
+#pragma unroll
+    for (int i = 0; i < PR; ++i)
+#pragma unroll
+        for (int j = 0; j < PC; ++j) {
+            const float *row = stage + ((r0 + i) * 8 + c0 + j) * RS + (E::bytes == 4 ? 8 : 4) * g;
+            if constexpr (E::bytes == 4) {
+                const f4 a = reinterpret_cast<const f4 *>(row)[0];
+                const f4 b = reinterpret_cast<const f4 *>(row)[1];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    out[u] += a[u];
+                    out[4 + u] += b[u];
+                }
+            } else {
+                const U16B w = *reinterpret_cast<const U16B *>(row);
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    out[2 * u] += __uint_as_float(w.w[u] << 16);
+                    out[2 * u + 1] += __uint_as_float(w.w[u] & 0xffff0000u);
+                }
+            }
+        }
+    wave_sync();
+    const bool valid = c < m;
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+        out[s] = (valid && slot_keep<D>(g, s)) ? out[s] : 0.f;
+}
+
 __device__ inline uint32_t pack_bf16x2(float lo, float hi)
 {
     typedef float f2 __attribute__((ext_vector_type(2)));
@@ -156,7 +217,7 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     // With a spare feature column (D not a multiple of 16), column D of V is
     // replaced by ones, so that column D of T, W and O carries T_D, W_D, O_D.
     constexpr bool PAD = D % 16 != 0;
-    using L = SmallLds<E, NT, D>;
+    using L = SmallLds<E, NT, D, GRID>;
     __shared__ __attribute__((aligned(16))) float lds_all[kWavesPerBlock * L::kPerWave];
     // The wave index is uniform across the wavefront; saying so keeps the
     // unit's base addresses in scalar registers.
@@ -168,7 +229,7 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     const int m = a.m;
     float *qbar = lds_all + wave * L::kPerWave;
     float *kbar = qbar + 16 * kLdStride;
-    float *scr = kbar + 16 * kLdStride;   // transpose scratch
+    float *scr = qbar + L::kRows;   // transpose scratch
     float *vec = scr + L::kStage;
 
     const int64_t base = unit * int64_t(N) * D;
@@ -220,26 +281,34 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 
     __builtin_amdgcn_sched_barrier(0);
 
-    // Landmark rows m..15 are padding: zero them so they contribute nothing.
-    for (int idx = lane; idx < (16 - m) * 32; idx += 64) {
-        const int r = m + idx / 32, f = idx % 32;
-        qbar[r * kLdStride + f] = 0.f;
-        kbar[r * kLdStride + f] = 0.f;
-    }
-    if constexpr (BFM) {
-        pool_to_lds<NT, D>([&](int tt, float *x) { unpack_bf8(qw[tt], x); }, qbar, a, g, c);
-        pool_to_lds<NT, D>([&](int tt, float *x) { unpack_bf8(kw[tt], x); }, kbar, a, g, c);
-    } else {
-        pool_to_lds<NT, D>([&](int tt, float *x) { for (int s = 0; s < 8; ++s) x[s] = qr[tt][s]; },
-                           qbar, a, g, c);
-        pool_to_lds<NT, D>([&](int tt, float *x) { for (int s = 0; s < 8; ++s) x[s] = kr[tt][s]; },
-                           kbar, a, g, c);
-    }
-    wave_sync();
     // Landmark rows in slot layout: kb[s] = Kbar[c][slot s of group g] (zero
-    // in overlapping slots), qb likewise.
+    // in overlapping slots), qb likewise (patch sums).
     float kb[8], qb[8];
-    {
+    if constexpr (GRID != kGridAny) {
+        if constexpr (BFM) {
+            pool_direct<E, NT, D, GRID>(qw, qbar, qb, m, g, c);
+            pool_direct<E, NT, D, GRID>(kw, qbar, kb, m, g, c);
+        } else {
+            pool_direct<E, NT, D, GRID>(qr, qbar, qb, m, g, c);
+            pool_direct<E, NT, D, GRID>(kr, qbar, kb, m, g, c);
+        }
+    } else {
+        // Landmark rows m..15 are padding: zero them so they contribute nothing.
+        for (int idx = lane; idx < (16 - m) * 32; idx += 64) {
+            const int r = m + idx / 32, f = idx % 32;
+            qbar[r * kLdStride + f] = 0.f;
+            kbar[r * kLdStride + f] = 0.f;
+        }
+        if constexpr (BFM) {
+            pool_to_lds<NT, D>([&](int tt, float *x) { unpack_bf8(qw[tt], x); }, qbar, a, g, c);
+            pool_to_lds<NT, D>([&](int tt, float *x) { unpack_bf8(kw[tt], x); }, kbar, a, g, c);
+        } else {
+            pool_to_lds<NT, D>([&](int tt, float *x) { for (int s = 0; s < 8; ++s) x[s] = qr[tt][s]; },
+                               qbar, a, g, c);
+            pool_to_lds<NT, D>([&](int tt, float *x) { for (int s = 0; s < 8; ++s) x[s] = kr[tt][s]; },
+                               kbar, a, g, c);
+        }
+        wave_sync();
         const f4 *kp = reinterpret_cast<const f4 *>(kbar + c * kLdStride + 8 * g);
         const f4 *qp = reinterpret_cast<const f4 *>(qbar + c * kLdStride + 8 * g);
         const f4 k0 = kp[0], k1 = kp[1], q0 = qp[0], q1 = qp[1];
