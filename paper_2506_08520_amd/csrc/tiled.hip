@@ -469,12 +469,15 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             const bf8 zs = split_tile(Z).hl;
             const SplitPair ZTs = transpose_split(zs, scr, g, c);
             const f4 Xq = mm16_hl(Aq, zs);
-            const SplitPair XTq = transpose_split(split_tile(Xq).hl, scr, g, c);
+            const bf8 xs = split_tile(Xq).hl;
+            const SplitPair XTq = transpose_split(xs, scr, g, c);
+            // Y2 = 15I - X (7I - X) = 15I - 28X' + 16X'^2, with X'^2 from the
+            // split terms already at hand (no split of 4 Y1).
+            const f4 X2 = mm16_hl(XTq, xs);
             f4 Y;
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                Y[i] = fmaf(Xq[i], -16.f, e28[i]);
-            Y = e15 - mm16_hl(XTq, split_tile(Y).hl);
+                Y[i] = fmaf(X2[i], 16.f, fmaf(Xq[i], -28.f, e15[i]));
             Y = e13q - mm16_hl(XTq, split_tile(Y).hl);
             Z = mm16_hl(ZTs, split_tile(Y).hl);
         }
@@ -517,7 +520,6 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 
     // ---- Steps 3 (G_L side), 6 and 7 per token tile: O = G_L^n W / O_D.
     const int olane = 4 * g * D + c;
-    const bool odd = c & 1;
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt) {
         f4 on[NCT];
@@ -552,19 +554,16 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                 x[i] = on[ct][i] * rcp[i];
             // O straight to HBM, row-major.
             if constexpr (BFM) {
-                // Lanes c and c^1 trade halves: the even lane writes rows 0 and
-                // 2 of features (c, c+1), the odd lane rows 1 and 3 of (c-1, c).
-                f4 nb;
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    nb[i] = dpp_xor1(x[i]);
-                const uint32_t p0 = odd ? pack_bf16x2(nb[1], x[1]) : pack_bf16x2(x[0], nb[0]);
-                const uint32_t p1 = odd ? pack_bf16x2(nb[3], x[3]) : pack_bf16x2(x[2], nb[2]);
-                const int fe = 16 * ct + (c & ~1);
-                if (fe < D) {
-                    uint16_t *dst = reinterpret_cast<uint16_t *>(ou) + (4 * g + int(odd)) * D + fe;
-                    *reinterpret_cast<uint32_t *>(dst + 16 * tt * D) = p0;
-                    *reinterpret_cast<uint32_t *>(dst + (16 * tt + 2) * D) = p1;
+                // Rows (0, 1) and (2, 3) of this lane's feature are converted
+                // in pairs (round to nearest even) and stored as 16-bit values.
+                const int f = 16 * ct + c;
+                if (f < D) {
+                    const uint32_t p01 = pack_bf16x2(x[0], x[1]), p23 = pack_bf16x2(x[2], x[3]);
+                    uint16_t *dst = reinterpret_cast<uint16_t *>(ou) + (16 * tt + 4 * g) * D + f;
+                    dst[0] = uint16_t(p01);
+                    dst[D] = uint16_t(p01 >> 16);
+                    dst[2 * D] = uint16_t(p23);
+                    dst[3 * D] = uint16_t(p23 >> 16);
                 }
             } else {
                 if (16 * ct + c < D) {
