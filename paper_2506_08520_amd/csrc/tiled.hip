@@ -1,7 +1,8 @@
 // MFMA-tiled PnP-Nystra kernel for small windows (N = 16, 32 or 64 tokens,
 // m <= 16 landmarks, d_h in {8, 12, ..., 28, 30, 32}): one wavefront computes one
-// (window, head) unit entirely in registers (register tiles in the D-layout of
-// tile_common.hpp), with LDS used only for a few small exchanges.  fp32 inputs
+// (window, head) unit in registers (register tiles in the D-layout of
+// tile_common.hpp), with LDS holding the pooling exchange and small
+// transposes.  fp32 inputs
 // run every contraction on v_mfma_f32_16x16x4f32; bf16 inputs run the
 // products with Q, K and V on v_mfma_f32_16x16x32_bf16, the fp32 partner
 // operand split into bf16 hi + lo terms, run the pseudo-inverse products as
@@ -55,16 +56,6 @@ struct SmallArgs {
     float inv_patch;   // 1 / tokens per pooling patch (a power of two)
     int lg_cols, lg_pr, lg_pc, lg_gc, free_bits;   // pooling grid (log2 sizes)
 };
-
-template <int GRID>
-__device__ inline void fix_grid(SmallArgs &a)
-{
-    if constexpr (GRID == kGrid2x2) {
-        a.lg_cols = 3; a.lg_pr = 1; a.lg_pc = 1; a.lg_gc = 2; a.free_bits = 1 | 8;
-    } else if constexpr (GRID == kGrid2x4) {
-        a.lg_cols = 3; a.lg_pr = 1; a.lg_pc = 2; a.lg_gc = 1; a.free_bits = 3 | 8;
-    }
-}
 
 int grid_of(const SmallArgs &a, int N)
 {
@@ -211,7 +202,6 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                    const typename E::T *__restrict__ v, typename E::T *__restrict__ o,
                    SmallArgs a)
 {
-    fix_grid<GRID>(a);
     constexpr int N = 16 * NT;
     constexpr int NCT = (D + 15) / 16;   // 16-wide feature tiles of V, T, W and O
     // With a spare feature column (D not a multiple of 16), column D of V is
