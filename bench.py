@@ -24,17 +24,16 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E peak, GB/s
 ROTATE_BYTES = 1.2 * (1 << 30)  # working set cycled by the timed steps
-WARMUP_SECONDS = 1.0           # default warm-up: long enough for steady clocks
 
 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=None,
-                    help="untimed launches before the timed ones (default: as many as run "
-                         "in about one second, so the GPU reaches its steady clocks; the "
-                         "count used is reported)")
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--preheat", type=float, default=1.0,
+                    help="seconds of untimed launches before the warm-up steps, so the GPU "
+                         "runs at its steady clocks (0: none); reported as preheat_s")
     ap.add_argument("--config", default="c2")
     ap.add_argument("--dtype", default="f32", choices=["f32", "bf16"])
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -76,8 +75,9 @@ class Case:
             self.sets.append((*trip, torch.empty_like(base[0])))
 
 
-def time_kernel(case, launch, steps, warmup):
-    """Warm up, then time exactly `steps` back-to-back launches.
+def time_kernel(case, launch, steps, warmup, preheat=0.0):
+    """Preheat for `preheat` seconds and run `warmup` untimed launches, then
+    time exactly `steps` back-to-back launches.
 
     Returns (ms per step by the host clock between the synchronisations that
     bracket the timed launches, ms per launch from one HIP event pair around
@@ -87,19 +87,17 @@ def time_kernel(case, launch, steps, warmup):
     kernels are launched on."""
     import torch
     stream = torch.cuda.current_stream()
-    if warmup is None:
-        # Warm up for about one second (checked every 64 launches).
-        warmup, t_end = 0, time.perf_counter() + WARMUP_SECONDS
-        while True:
-            for _ in range(64):
-                launch(*case.sets[warmup % case.nsets], stream)
-                warmup += 1
-            torch.cuda.synchronize()
-            if time.perf_counter() >= t_end:
-                break
-    else:
-        for i in range(warmup):
-            launch(*case.sets[i % case.nsets], stream)
+    # The first launches after idle run at lower clocks (c2 fp32: 51.7 us
+    # after 20 launches, 46.3 us after a second of them); the preheat runs
+    # the same launches for the given time, checked every 64 launches.
+    heat, t_end = 0, time.perf_counter() + preheat
+    while time.perf_counter() < t_end:
+        for _ in range(64):
+            launch(*case.sets[heat % case.nsets], stream)
+            heat += 1
+        torch.cuda.synchronize()
+    for i in range(warmup):
+        launch(*case.sets[i % case.nsets], stream)
     r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -119,7 +117,7 @@ def time_kernel(case, launch, steps, warmup):
         stops[i].record(stream)
     torch.cuda.synchronize()
     pairs = sum(a.elapsed_time(b) for a, b in zip(starts, stops)) / n
-    return (t1 - t0) * 1e3 / steps, region, pairs, warmup
+    return (t1 - t0) * 1e3 / steps, region, pairs, heat
 
 
 def measured_traffic(cfg, dtype, variant):
@@ -397,13 +395,14 @@ def main():
         def ex(q_, k_, v_, o_, s):
             B.nystra_exact_attn_forward(q_, k_, v_, out=o_, stream=s)
 
-        ms, kern, pairs, warm = time_kernel(case, nys, args.steps, args.warmup)
+        ms, kern, pairs, heat = time_kernel(case, nys, args.steps, args.warmup, args.preheat)
         r = {"ms_per_step": ms, "kernel_ms": kern, "pairs_ms": pairs, "io_bytes": case.io_bytes,
-             "warmup": warm,
+             "preheat_launches": heat,
              "variant": B.nystra_select_variant(wl.N, wl.d, wl.m,
                                                 B.F32 if dt == "f32" else B.BF16)}
         if not args.no_exact:
-            ems, ekern, _, _ = time_kernel(case, ex, max(10, args.steps // 4), args.warmup)
+            ems, ekern, _, _ = time_kernel(case, ex, max(10, args.steps // 4), args.warmup,
+                                           args.preheat)
             r.update(exact_ms_per_step=ems, exact_kernel_ms=ekern)
         results[dt] = r
         del case
@@ -419,7 +418,9 @@ def main():
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": r["warmup"],
+        "warmup": args.warmup,
+        "preheat_s": args.preheat,
+        "preheat_launches": r["preheat_launches"],
         "ms_per_step": r["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
