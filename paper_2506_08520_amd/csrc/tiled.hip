@@ -59,9 +59,11 @@ struct SmallArgs {
 
 int grid_of(const SmallArgs &a, int N)
 {
-    if (N == 64 && a.lg_cols == 3 && a.lg_pr == 1 && a.lg_pc == 1 && a.lg_gc == 2 && a.free_bits == 9)
+    if (N == 64 && a.m == 16 && a.lg_cols == 3 && a.lg_pr == 1 && a.lg_pc == 1 && a.lg_gc == 2 &&
+        a.free_bits == 9)
         return kGrid2x2;
-    if (N == 64 && a.lg_cols == 3 && a.lg_pr == 1 && a.lg_pc == 2 && a.lg_gc == 1 && a.free_bits == 11)
+    if (N == 64 && a.m == 8 && a.lg_cols == 3 && a.lg_pr == 1 && a.lg_pc == 2 && a.lg_gc == 1 &&
+        a.free_bits == 11)
         return kGrid2x4;
     return kGridAny;
 }
@@ -216,7 +218,9 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     const int64_t unit = int64_t(blockIdx.x) * kWavesPerBlock + wave;
     if (unit >= a.units)
         return;   // whole wavefront; the kernel has no block-level barrier
-    const int m = a.m;
+    // The fixed grids imply m (16 for 2 x 2 patches, 8 for 2 x 4), so the
+    // landmark masks fold away.
+    const int m = GRID == kGrid2x2 ? 16 : GRID == kGrid2x4 ? 8 : a.m;
     float *qbar = lds_all + wave * L::kPerWave;
     float *kbar = qbar + 16 * kLdStride;
     float *scr = qbar + L::kRows;   // transpose scratch
