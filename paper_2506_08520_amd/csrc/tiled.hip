@@ -197,7 +197,9 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi)
 // waves instead of four, bf16 33.8 -> 29.9 us at four instead of six); on
 // L2-resident inputs the computation alone runs at the same speed from three
 // to six waves.
-template <class E, int NT, int D, bool BFM, int GRID>
+// KF > 0 fixes the number of pseudo-inverse iterations at compile time (the
+// loop is unrolled); KF = 0 takes it from SmallArgs.
+template <class E, int NT, int D, bool BFM, int GRID, int KF>
 __global__ void __launch_bounds__(64 * kWavesPerBlock)
 __attribute__((amdgpu_waves_per_eu(1, BFM ? 4 : 3)))
 tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__restrict__ k,
@@ -459,7 +461,7 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         // left factors come in both k orders, X'^T and Z^T by moving the split
         // terms of X' and Z through LDS.
         const SplitPair Aq = both_orders(split_tile(ATq).hl);
-        for (int it = 0; it < a.iters; ++it) {
+        auto step = [&]() {
             const bf8 zs = split_tile(Z).hl;
             const SplitPair ZTs = transpose_split(zs, scr, g, c);
             const f4 Xq = mm16_hl(Aq, zs);
@@ -474,11 +476,19 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                 Y[i] = fmaf(X2[i], 16.f, fmaf(Xq[i], -28.f, e15[i]));
             Y = e13q - mm16_hl(XTq, split_tile(Y).hl);
             Z = mm16_hl(ZTs, split_tile(Y).hl);
+        };
+        if constexpr (KF > 0) {
+#pragma unroll
+            for (int it = 0; it < KF; ++it)
+                step();
+        } else {
+            for (int it = 0; it < a.iters; ++it)
+                step();
         }
-        if (a.iters > 0)
+        if (KF > 0 || a.iters > 0)
             ZT = transpose16(Z, scr, g, c);
     } else {
-        for (int it = 0; it < a.iters; ++it) {
+        auto step = [&]() {
             const f4 Xq = mm16(ATq, Z);
             const f4 XTq = transpose16(Xq, scr, g, c);
             f4 Y;
@@ -489,6 +499,14 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             Y = e13q - mm16(XTq, Y);
             Z = mm16(ZT, Y);
             ZT = transpose16(Z, scr, g, c);
+        };
+        if constexpr (KF > 0) {
+#pragma unroll
+            for (int it = 0; it < KF; ++it)
+                step();
+        } else {
+            for (int it = 0; it < a.iters; ++it)
+                step();
         }
     }
 
@@ -580,11 +598,11 @@ int ilog2(int x)
     return r;
 }
 
-template <class E, int NT, int D, int GRID = kGridAny>
+template <class E, int NT, int D, int GRID = kGridAny, int KF = 0>
 void launch_small(const Problem &p, const SmallArgs &a, hipStream_t stream)
 {
     const unsigned blocks = unsigned((p.units + kWavesPerBlock - 1) / kWavesPerBlock);
-    hipLaunchKernelGGL((tiled_small_kernel<E, NT, D, E::bytes == 2, GRID>), dim3(blocks),
+    hipLaunchKernelGGL((tiled_small_kernel<E, NT, D, E::bytes == 2, GRID, KF>), dim3(blocks),
                        dim3(64 * kWavesPerBlock),
                        0, stream, static_cast<const typename E::T *>(p.q),
                        static_cast<const typename E::T *>(p.k),
@@ -600,8 +618,19 @@ void launch_small_d(const Problem &p, const SmallArgs &a, hipStream_t stream)
     case 32: launch_small<E, 2, D>(p, a, stream); break;
     default:
         switch (grid_of(a, p.N)) {
-        case kGrid2x2: launch_small<E, 4, D, kGrid2x2>(p, a, stream); break;
-        case kGrid2x4: launch_small<E, 4, D, kGrid2x4>(p, a, stream); break;
+        // K = 6, the iteration count of the paper's experiments, unrolled.
+        case kGrid2x2:
+            if (a.iters == 6)
+                launch_small<E, 4, D, kGrid2x2, 6>(p, a, stream);
+            else
+                launch_small<E, 4, D, kGrid2x2>(p, a, stream);
+            break;
+        case kGrid2x4:
+            if (a.iters == 6)
+                launch_small<E, 4, D, kGrid2x4, 6>(p, a, stream);
+            else
+                launch_small<E, 4, D, kGrid2x4>(p, a, stream);
+            break;
         default: launch_small<E, 4, D>(p, a, stream); break;
         }
         break;
