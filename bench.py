@@ -39,6 +39,8 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-exact", action="store_true", help="skip the exact-attention timing")
     ap.add_argument("--no-alt", action="store_true", help="skip the other-dtype run")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the same-traffic elementwise kernel (the practical HBM ceiling)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the benchmark line: time PnP-Nystra and exact attention "
@@ -404,6 +406,17 @@ def main():
             ems, ekern, _, _ = time_kernel(case, ex, max(10, args.steps // 4), args.warmup,
                                            args.preheat)
             r.update(exact_ms_per_step=ems, exact_kernel_ms=ekern)
+        if not args.no_ceiling:
+            # The practical HBM ceiling for this traffic: one elementwise kernel
+            # that reads Q, K and V and writes O once (O = Q + K * V), on the
+            # same rotating buffers and stream -- the same bytes as one step,
+            # with no arithmetic to speak of.
+            def same_traffic(q_, k_, v_, o_, s):
+                torch.addcmul(q_, k_, v_, out=o_)
+
+            _, ckern, _, _ = time_kernel(case, same_traffic, args.steps, args.warmup,
+                                         min(args.preheat, 0.3))
+            r["ceiling_kernel_ms"] = ckern
         results[dt] = r
         del case
         torch.cuda.empty_cache()
@@ -438,6 +451,12 @@ def main():
     }
     if "exact_kernel_ms" in r:
         line["speedup_vs_exact"] = r["exact_kernel_ms"] / r["kernel_ms"]
+    if "ceiling_kernel_ms" in r:
+        ceil_gbs = r["io_bytes"] / (r["ceiling_kernel_ms"] * 1e-3) / 1e9
+        line["same_traffic_ceiling"] = {
+            "kernel": "torch.addcmul: reads Q, K, V and writes O once, the bytes of one step",
+            "kernel_ms": r["ceiling_kernel_ms"], "achieved": ceil_gbs, "unit": "GB/s",
+            "frac": ceil_gbs / HBM_PEAK_GBS, "nystrom_over_ceiling": achieved / ceil_gbs}
     line["kernel_ms"] = r["kernel_ms"]
     line["kernel_ms_event_pairs"] = r["pairs_ms"]
     line["variant"] = "mfma-tiled" if r["variant"] == 2 else "generic"
@@ -450,6 +469,10 @@ def main():
             "kernel_ms": rr["kernel_ms"], "achieved_GBs": ach, "frac": ach / HBM_PEAK_GBS,
             "speedup_vs_exact": (rr["exact_kernel_ms"] / rr["kernel_ms"]
                                  if "exact_kernel_ms" in rr else None)}
+        if "ceiling_kernel_ms" in rr:
+            cg = rr["io_bytes"] / (rr["ceiling_kernel_ms"] * 1e-3) / 1e9
+            line[f"{dt}_storage"]["same_traffic_ceiling_frac"] = cg / HBM_PEAK_GBS
+            line[f"{dt}_storage"]["nystrom_over_ceiling"] = ach / cg
     if args.copy_mib > 0:
         n = args.copy_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")

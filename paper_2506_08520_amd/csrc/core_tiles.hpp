@@ -128,8 +128,9 @@ constexpr int table_den() { return 16 * MT * kTS; }
 //   tden  T_D of landmark l (sum of row l of G_U^n)
 // Kbar must be complete in LDS (LargeLds::kbar, pitch kTS) and visible to all
 // waves.  On return, after a workgroup barrier, W and W_D are in the table at
-// LargeLds::wb (W_D at offset table_den<MT>()).
-template <int MT, int D, bool BFM>
+// LargeLds::wb (W_D at offset table_den<MT>()).  FULL says m = 16 MT (every
+// landmark slot real), which folds the masks.
+template <int MT, int D, bool BFM, bool FULL = false>
 __device__ inline void landmark_core(float *lds, const float (&qb)[8], float mu,
                                               const f4 (&T)[2], float tden, int m, int iters,
                                               float s2, int lt, int lane)
@@ -141,7 +142,7 @@ __device__ inline void landmark_core(float *lds, const float (&qb)[8], float mu,
     float *Tb = lds + L::tb, *Wb = lds + L::wb;
     const int g = lane >> 4, c = lane & 15;
     const int l = 16 * lt + c;
-    const bool lval = l < m;
+    const bool lval = FULL || l < m;
 
     // ---- Step 2: this wave's row tile of A = G_A^n, in transposed form:
     // ALT[j] lane (g,c): A[16lt + c][16j + 4g + i].
@@ -157,8 +158,8 @@ __device__ inline void landmark_core(float *lds, const float (&qb)[8], float mu,
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-            ALT[j][i] = (lval && 16 * j + 4 * g + i < m) ? fast_exp2(fmaf(s2, acc[i], -mu))
-                                                         : 0.f;
+            ALT[j][i] = (lval && (FULL || 16 * j + 4 * g + i < m))
+                            ? fast_exp2(fmaf(s2, acc[i], -mu)) : 0.f;
     }
 
     // ---- Step 4: Z_0 = A^T / (||A||_1 ||A||_inf).

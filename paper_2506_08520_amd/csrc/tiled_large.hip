@@ -36,7 +36,8 @@ struct LargeArgs {
     int cols, pr, pc, gc;   // pooling grid
 };
 
-template <class E, int MT, int D, bool BFM>
+// FULL: m = 16 MT, so every landmark slot is real and the masks fold away.
+template <class E, int MT, int D, bool BFM, bool FULL>
 __global__ void __launch_bounds__(64 * MT)
 tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__restrict__ k,
                    const typename E::T *__restrict__ v, typename E::T *__restrict__ o,
@@ -50,9 +51,9 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     const int lt = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int g = lane >> 4, c = lane & 15;
     float *vec = lds + L::vec + 64 * lt;
-    const int m = a.m, N = a.N, NT = a.N >> 4;
+    const int m = FULL ? 16 * MT : a.m, N = a.N, NT = a.N >> 4;
     const int l = 16 * lt + c;            // this lane's landmark
-    const bool lval = l < m;
+    const bool lval = FULL || l < m;
     const int64_t base = int64_t(blockIdx.x) * N * d;
     const typename E::T *qu = q + base, *ku = k + base, *vu = v + base;
     typename E::T *ou = o + base;
@@ -141,16 +142,15 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 #pragma unroll
             for (int ct = 0; ct < 2; ++ct) {
                 const int f = 16 * ct + c;
+                // Columns past d repeat column d - 1: they reach only columns
+                // of T, W and O that are never stored (T_D is summed apart).
+                const int64_t vrow = int64_t(16 * tt + 4 * g) * d + min(f, d - 1);
 #pragma unroll
                 for (int s = 0; s < 4; ++s) {
-                    const int64_t idx = int64_t(16 * tt + 4 * g + s) * d + min(f, d - 1);
-                    if constexpr (BFM) {
-                        const uint16_t x = vu16[idx];
-                        vh[u][ct][s] = f < d ? x : uint16_t(0);
-                    } else {
-                        const float x = E::load(vu, idx);
-                        vr[u][ct][s] = f < d ? x : 0.f;
-                    }
+                    if constexpr (BFM)
+                        vh[u][ct][s] = vu16[vrow + s * d];
+                    else
+                        vr[u][ct][s] = E::load(vu, vrow + s * d);
                 }
             }
         }
@@ -226,7 +226,7 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     tden = sum_groups(tden);   // T_D of landmark l
     __syncthreads();           // Kbar complete
 
-    landmark_core<MT, D, BFM>(lds, qb, mu, T, tden, m, a.iters, a.s2, lt, lane);
+    landmark_core<MT, D, BFM, FULL>(lds, qb, mu, T, tden, m, a.iters, a.s2, lt, lane);
     constexpr int TDo = table_den<MT>();
     float *Wb = lds + L::wb;
 
@@ -300,7 +300,7 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                 glT[kk] = acc;
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    if (16 * kk + 4 * g + i < m)
+                    if (FULL || 16 * kk + 4 * g + i < m)
                         ml = fmaxf(ml, acc[i]);
             }
             ml = a.s2 * max_groups(ml);
@@ -309,7 +309,7 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             for (int kk = 0; kk < MT; ++kk)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const float e = (16 * kk + 4 * g + i < m)
+                    const float e = (FULL || 16 * kk + 4 * g + i < m)
                                         ? fast_exp2(fmaf(a.s2, glT[kk][i], -ml)) : 0.f;
                     glT[kk][i] = e;
                     od = fmaf(e, wdv[kk][i], od);
@@ -350,9 +350,22 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                 }
                 const int f = 16 * ct + c;
                 if (f < d) {
+                    const int64_t orow = int64_t(16 * tt + 4 * g) * d + f;
+                    if constexpr (E::bytes == 2) {
+                        // rows (0, 1) and (2, 3) converted in pairs (round to
+                        // nearest even), stored as 16-bit values
+                        uint16_t *o16 = reinterpret_cast<uint16_t *>(ou) + orow;
+                        const uint32_t p01 = cvt_bf16x2(on[0] * rcp[0], on[1] * rcp[1]);
+                        const uint32_t p23 = cvt_bf16x2(on[2] * rcp[2], on[3] * rcp[3]);
+                        o16[0] = uint16_t(p01);
+                        o16[d] = uint16_t(p01 >> 16);
+                        o16[2 * d] = uint16_t(p23);
+                        o16[3 * d] = uint16_t(p23 >> 16);
+                    } else {
 #pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        E::store(ou, int64_t(16 * tt + 4 * g + i) * d + f, on[i] * rcp[i]);
+                        for (int i = 0; i < 4; ++i)
+                            E::store(ou, orow + i * d, on[i] * rcp[i]);
+                    }
                 }
             }
         }
@@ -360,8 +373,8 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 }
 
 // bf16 inputs with N % 32 == 0 take the bf16 matrix-core path.
-template <class E, int MT, int D>
-void launch_large(const Problem &p, const LargeArgs &a, hipStream_t stream)
+template <class E, int MT, int D, bool FULL>
+void launch_large_f(const Problem &p, const LargeArgs &a, hipStream_t stream)
 {
     const size_t lds = size_t(LargeLds<MT>::total) * sizeof(float);
     const auto *q = static_cast<const typename E::T *>(p.q);
@@ -370,11 +383,20 @@ void launch_large(const Problem &p, const LargeArgs &a, hipStream_t stream)
     auto *o = static_cast<typename E::T *>(p.o);
     const dim3 grid(unsigned(p.units)), block(64 * MT);
     if (E::bytes == 2 && p.N % 32 == 0)
-        hipLaunchKernelGGL((tiled_large_kernel<E, MT, D, E::bytes == 2>), grid, block, lds,
-                           stream, q, k, v, o, a);
+        hipLaunchKernelGGL((tiled_large_kernel<E, MT, D, E::bytes == 2, FULL>), grid, block,
+                           lds, stream, q, k, v, o, a);
     else
-        hipLaunchKernelGGL((tiled_large_kernel<E, MT, D, false>), grid, block, lds, stream, q,
-                           k, v, o, a);
+        hipLaunchKernelGGL((tiled_large_kernel<E, MT, D, false, FULL>), grid, block, lds,
+                           stream, q, k, v, o, a);
+}
+
+template <class E, int MT, int D>
+void launch_large(const Problem &p, const LargeArgs &a, hipStream_t stream)
+{
+    if (p.m == 16 * MT)
+        launch_large_f<E, MT, D, true>(p, a, stream);
+    else
+        launch_large_f<E, MT, D, false>(p, a, stream);
 }
 
 template <class E, int D>
