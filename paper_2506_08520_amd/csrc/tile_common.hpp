@@ -327,6 +327,20 @@ __device__ inline bf8 load_chunk8_bf8(const uint16_t *row, int g)
     return __builtin_bit_cast(bf8, u);
 }
 
+// A raw bf16 chunk (load_row8_bf16 at chunk_start) with the slots that a
+// lower lane group carries zeroed: the load_chunk8_bf8 result, applied after
+// the load so that a prefetched chunk is not waited for at its issue.
+template <int D>
+__device__ inline bf8 mask_chunk8_bf8(bf8 x, int g)
+{
+    U16B u = __builtin_bit_cast(U16B, x);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        if (!slot_valid<D>(g, 2 * j))
+            u.w[j] = 0u;
+    return __builtin_bit_cast(bf8, u);
+}
+
 // Slot s of lane group g carries a feature that no lower group carries; the
 // chunk of the last, partial group (f0 = D - 8) overlaps the one below it.
 // Equivalent to slot_valid, written so that D-dependent parts fold.

@@ -127,18 +127,26 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     float tden = 0.f;    // this lane's share of T_D of landmark l
     float mrun = -INFINITY;   // running max of S_U[l][.] (unscaled logits)
     const uint16_t *vu16 = reinterpret_cast<const uint16_t *>(vu);
-    for (int t0 = 0; t0 < NT; t0 += kGroup) {
-        float kr[kGroup][8], vr[kGroup][2][4];
-        bf8 kw[kGroup];
-        uint16_t vh[kGroup][2][4];
+    // Key groups are software-pipelined: the loads of group t0 + kGroup are
+    // issued before group t0 is computed (past the end they repeat the last
+    // tile and go unused).  Chunks are loaded raw and their overlapping slots
+    // zeroed when the group is consumed, so no instruction waits on a load
+    // at its issue.
+    float kr[kGroup][8], vr[kGroup][2][4], krn[kGroup][8], vrn[kGroup][2][4];
+    bf8 kw[kGroup], kwn[kGroup];
+    uint16_t vh[kGroup][2][4], vhn[kGroup][2][4];
+    auto load_group = [&](int t0, float (&kr_)[kGroup][8], bf8 (&kw_)[kGroup],
+                          float (&vr_)[kGroup][2][4], uint16_t (&vh_)[kGroup][2][4]) {
 #pragma unroll
         for (int u = 0; u < kGroup; ++u) {
             const int tt = min(t0 + u, NT - 1);
             const int64_t row = int64_t(16 * tt + c) * d;
             if constexpr (BFM)
-                kw[u] = load_chunk8_bf8<D>(ku16 + row, g);
-            else
-                load_chunk8<E, D>(ku + row, g, kr[u]);
+                kw_[u] = load_row8_bf16(ku16 + row + chunk_start<D>(g));
+            else if constexpr (E::bytes == 4)
+                load_row8<D>(ku + row + chunk_start<D>(g), kr_[u]);
+            else   // bf16 values through the fp32 path: unpacked (and masked) here
+                load_chunk8<E, D>(ku + row, g, kr_[u]);
 #pragma unroll
             for (int ct = 0; ct < 2; ++ct) {
                 const int f = 16 * ct + c;
@@ -148,10 +156,24 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 #pragma unroll
                 for (int s = 0; s < 4; ++s) {
                     if constexpr (BFM)
-                        vh[u][ct][s] = vu16[vrow + s * d];
+                        vh_[u][ct][s] = vu16[vrow + s * d];
                     else
-                        vr[u][ct][s] = E::load(vu, vrow + s * d);
+                        vr_[u][ct][s] = E::load(vu, vrow + s * d);
                 }
+            }
+        }
+    };
+    load_group(0, kr, kw, vr, vh);
+    for (int t0 = 0; t0 < NT; t0 += kGroup) {
+        load_group(t0 + kGroup, krn, kwn, vrn, vhn);
+#pragma unroll
+        for (int u = 0; u < kGroup; ++u) {
+            if constexpr (BFM) {
+                kw[u] = mask_chunk8_bf8<D>(kw[u], g);
+            } else {
+#pragma unroll
+                for (int s = 0; s < 8; ++s)
+                    kr[u][s] = slot_valid<D>(g, s) ? kr[u][s] : 0.f;
             }
         }
         // Logits of the group (a repeated last tile leaves the maximum unchanged
@@ -221,6 +243,20 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                         T[ct] = mfma4(e[s], vr[u][ct][s], T[ct]);
             }
         }
+#pragma unroll
+        for (int u = 0; u < kGroup; ++u) {
+            kw[u] = kwn[u];
+#pragma unroll
+            for (int x = 0; x < 8; ++x)
+                kr[u][x] = krn[u][x];
+#pragma unroll
+            for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+                for (int x = 0; x < 4; ++x) {
+                    vr[u][ct][x] = vrn[u][ct][x];
+                    vh[u][ct][x] = vhn[u][ct][x];
+                }
+        }
     }
     const float mu = a.s2 * mrun;   // m_U of landmark l (base-2 units)
     tden = sum_groups(tden);   // T_D of landmark l
@@ -266,19 +302,27 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     }
     const uint16_t *qu16 = reinterpret_cast<const uint16_t *>(qu);
     // Token tiles of this wave: lt, lt + MT, ...; the Q rows of kQGroup tiles
-    // are loaded together.
+    // loaded together; the next group's rows are requested before this group
+    // is computed (as in the key pass).  The chunks stay unmasked: the
+    // overlapping slots meet zeros on the Kbar side.
     constexpr int kQGroup = 2;
-    for (int t0 = lt; t0 < NT; t0 += kQGroup * MT) {
-        float qg[kQGroup][8];
-        bf8 qw[kQGroup];
+    float qg[kQGroup][8], qgn[kQGroup][8];
+    bf8 qw[kQGroup], qwn[kQGroup];
+    auto load_q = [&](int t0, float (&qg_)[kQGroup][8], bf8 (&qw_)[kQGroup]) {
 #pragma unroll
         for (int u = 0; u < kQGroup; ++u) {
             const int64_t row = int64_t(16 * min(t0 + u * MT, NT - 1) + c) * d;
             if constexpr (BFM)
-                qw[u] = load_chunk8_bf8<D>(qu16 + row, g);
+                qw_[u] = load_row8_bf16(qu16 + row + chunk_start<D>(g));
+            else if constexpr (E::bytes == 4)
+                load_row8<D>(qu + row + chunk_start<D>(g), qg_[u]);
             else
-                load_chunk8<E, D>(qu + row, g, qg[u]);
+                load_chunk8<E, D>(qu + row, g, qg_[u]);
         }
+    };
+    load_q(lt, qg, qw);
+    for (int t0 = lt; t0 < NT; t0 += kQGroup * MT) {
+        load_q(t0 + kQGroup * MT, qgn, qwn);
 #pragma unroll
         for (int u = 0; u < kQGroup; ++u) {
             const int tt = t0 + u * MT;
@@ -368,6 +412,13 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                     }
                 }
             }
+        }
+#pragma unroll
+        for (int u = 0; u < kQGroup; ++u) {
+            qw[u] = qwn[u];
+#pragma unroll
+            for (int x = 0; x < 8; ++x)
+                qg[u][x] = qgn[u][x];
         }
     }
 }
