@@ -212,12 +212,13 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     // replaced by ones, so that column D of T, W and O carries T_D, W_D, O_D.
     constexpr bool PAD = D % 16 != 0;
     using L = SmallLds<E, NT, D, GRID>;
-    __shared__ __attribute__((aligned(16))) float lds_all[kWavesPerBlock * L::kPerWave];
+    // L::kPerWave floats per wave of the workgroup (sized at launch)
+    extern __shared__ __attribute__((aligned(16))) float lds_all[];
     // The wave index is uniform across the wavefront; saying so keeps the
     // unit's base addresses in scalar registers.
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
     const int g = lane >> 4, c = lane & 15;
-    const int64_t unit = int64_t(blockIdx.x) * kWavesPerBlock + wave;
+    const int64_t unit = int64_t(blockIdx.x) * (blockDim.x >> 6) + wave;
     if (unit >= a.units)
         return;   // whole wavefront; the kernel has no block-level barrier
     // The fixed grids imply m (16 for 2 x 2 patches, 8 for 2 x 4), so the
@@ -598,13 +599,19 @@ int ilog2(int x)
     return r;
 }
 
+// Below this many units, four-wave workgroups would leave compute units idle
+// (256 on the MI355X): each unit then gets a workgroup of its own, so that the
+// units spread over the whole chip.
+constexpr int64_t kFewUnits = 4 * 256;
+
 template <class E, int NT, int D, int GRID = kGridAny, int KF = 0>
 void launch_small(const Problem &p, const SmallArgs &a, hipStream_t stream)
 {
-    const unsigned blocks = unsigned((p.units + kWavesPerBlock - 1) / kWavesPerBlock);
+    const int wpb = p.units < kFewUnits ? 1 : kWavesPerBlock;
+    const unsigned blocks = unsigned((p.units + wpb - 1) / wpb);
+    const size_t lds = size_t(wpb) * SmallLds<E, NT, D, GRID>::kPerWave * sizeof(float);
     hipLaunchKernelGGL((tiled_small_kernel<E, NT, D, E::bytes == 2, GRID, KF>), dim3(blocks),
-                       dim3(64 * kWavesPerBlock),
-                       0, stream, static_cast<const typename E::T *>(p.q),
+                       dim3(64 * wpb), lds, stream, static_cast<const typename E::T *>(p.q),
                        static_cast<const typename E::T *>(p.k),
                        static_cast<const typename E::T *>(p.v),
                        static_cast<typename E::T *>(p.o), a);
