@@ -215,31 +215,62 @@ split_keys_kernel(const typename E::T *__restrict__ k, const typename E::T *__re
     // Wave w takes the tile pairs w, w + 4, ...; the second tile of a pair past
     // the chunk's end (fp32 path with an odd tile count) repeats the first and
     // is not accumulated.
-    for (int t0 = 2 * w; t0 < NT; t0 += 2 * kWaves) {
-        float kr[2][8], vr[2][NCT][4];
-        bf8 kw[2];
-        uint16_t vh[2][NCT][4];
+    // The pairs are software-pipelined: the next pair's K and V rows are
+    // requested before this pair is computed (past the end they repeat the
+    // last tile, unused).  Rows arrive raw; masks and the ones column are
+    // applied when the pair is consumed, so no instruction waits on a load at
+    // its issue.
+    float kr[2][8], vr[2][NCT][4], krn[2][8], vrn[2][NCT][4];
+    bf8 kw[2], kwn[2];
+    uint16_t vh[2][NCT][4], vhn[2][NCT][4];
+    auto load_pair = [&](int t0, float (&kr_)[2][8], bf8 (&kw_)[2], float (&vr_)[2][NCT][4],
+                         uint16_t (&vh_)[2][NCT][4]) {
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
             const int tt = min(t0 + u, NT - 1);
             const int64_t row = int64_t(k0 + 16 * tt + c) * d;
             if constexpr (BFM)
-                kw[u] = load_chunk8_bf8<D>(ku16 + row, g);
-            else
-                load_chunk8<E, D>(ku + row, g, kr[u]);
+                kw_[u] = load_row8_bf16(ku16 + row + chunk_start<D>(g));
+            else if constexpr (E::bytes == 4)
+                load_row8<D>(ku + row + chunk_start<D>(g), kr_[u]);
+            else   // bf16 values through the fp32 path: unpacked (and masked) here
+                load_chunk8<E, D>(ku + row, g, kr_[u]);
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) {
+                const int f = 16 * ct + c;
+                const int64_t vrow = int64_t(k0 + 16 * tt + 4 * g) * d + min(f, d - 1);
+#pragma unroll
+                for (int s = 0; s < 4; ++s) {
+                    if constexpr (BFM)
+                        vh_[u][ct][s] = vu16[vrow + s * d];
+                    else
+                        vr_[u][ct][s] = E::load(vu, vrow + s * d);
+                }
+            }
+        }
+    };
+    load_pair(2 * w, kr, kw, vr, vh);
+    for (int t0 = 2 * w; t0 < NT; t0 += 2 * kWaves) {
+        load_pair(t0 + 2 * kWaves, krn, kwn, vrn, vhn);
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            if constexpr (BFM) {
+                kw[u] = mask_chunk8_bf8<D>(kw[u], g);
+            } else if constexpr (E::bytes == 4) {
+#pragma unroll
+                for (int s = 0; s < 8; ++s)
+                    kr[u][s] = slot_valid<D>(g, s) ? kr[u][s] : 0.f;
+            }
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) {
                 const int f = 16 * ct + c;
 #pragma unroll
                 for (int s = 0; s < 4; ++s) {
-                    const int64_t idx = int64_t(k0 + 16 * tt + 4 * g + s) * d + min(f, d - 1);
-                    if constexpr (BFM) {
-                        const uint16_t x = vu16[idx];
-                        vh[u][ct][s] = f < d ? x : uint16_t(kOnes && f == d ? 0x3F80u : 0u);
-                    } else {
-                        const float x = E::load(vu, idx);
-                        vr[u][ct][s] = f < d ? x : (kOnes && f == d ? 1.f : 0.f);
-                    }
+                    if constexpr (BFM)
+                        vh[u][ct][s] = f < d ? vh[u][ct][s]
+                                             : uint16_t(kOnes && f == d ? 0x3F80u : 0u);
+                    else
+                        vr[u][ct][s] = f < d ? vr[u][ct][s] : (kOnes && f == d ? 1.f : 0.f);
                 }
             }
         }
@@ -326,6 +357,20 @@ split_keys_kernel(const typename E::T *__restrict__ k, const typename E::T *__re
                             T[j][ct] = mfma4(e[s], vr[u][ct][s], T[j][ct]);
                 }
             }
+        }
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            kw[u] = kwn[u];
+#pragma unroll
+            for (int x = 0; x < 8; ++x)
+                kr[u][x] = krn[u][x];
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                for (int x = 0; x < 4; ++x) {
+                    vr[u][ct][x] = vrn[u][ct][x];
+                    vh[u][ct][x] = vhn[u][ct][x];
+                }
         }
     }
 
@@ -545,17 +590,26 @@ split_query_kernel(const typename E::T *__restrict__ q, typename E::T *__restric
 
     auto tiles = [&](auto full) {
         constexpr bool FULL = decltype(full)::value;   // m == 16 MT: no landmark masks
-        for (int t0 = w; t0 < NT; t0 += kQGroup * kWaves) {
-            float qg[kQGroup][8];
-            bf8 qw[kQGroup];
+        // Software-pipelined as in the keys pass: the next group's Q rows are
+        // requested before this group is computed.  The chunks stay unmasked:
+        // the overlapping slots meet zeros on the Kbar side.
+        float qg[kQGroup][8], qgn[kQGroup][8];
+        bf8 qw[kQGroup], qwn[kQGroup];
+        auto load_q = [&](int t0, float (&qg_)[kQGroup][8], bf8 (&qw_)[kQGroup]) {
 #pragma unroll
             for (int u = 0; u < kQGroup; ++u) {
                 const int64_t row = int64_t(q0 + 16 * min(t0 + u * kWaves, NT - 1) + c) * d;
                 if constexpr (BFM)
-                    qw[u] = load_chunk8_bf8<D>(qu16 + row, g);
+                    qw_[u] = load_row8_bf16(qu16 + row + chunk_start<D>(g));
+                else if constexpr (E::bytes == 4)
+                    load_row8<D>(qu + row + chunk_start<D>(g), qg_[u]);
                 else
-                    load_chunk8<E, D>(qu + row, g, qg[u]);
+                    load_chunk8<E, D>(qu + row, g, qg_[u]);
             }
+        };
+        load_q(w, qg, qw);
+        for (int t0 = w; t0 < NT; t0 += kQGroup * kWaves) {
+            load_q(t0 + kQGroup * kWaves, qgn, qwn);
 #pragma unroll
             for (int u = 0; u < kQGroup; ++u) {
                 const int tt = t0 + u * kWaves;
@@ -660,6 +714,13 @@ split_query_kernel(const typename E::T *__restrict__ q, typename E::T *__restric
                     if (p0 + lane < kPieces)
                         dst[p0 + lane] = src[p0 + lane];
                 wave_sync();
+            }
+#pragma unroll
+            for (int u = 0; u < kQGroup; ++u) {
+                qw[u] = qwn[u];
+#pragma unroll
+                for (int x = 0; x < 8; ++x)
+                    qg[u][x] = qgn[u][x];
             }
         }
     };
