@@ -452,3 +452,19 @@ def test_empty_batch_is_noop():
     q = torch.empty((0, 6, 64, 30), device="cuda")
     o = B.nystra_attn_forward(q, q, q, 16)
     assert o.numel() == 0
+
+
+# The small-window kernel launches one-wave workgroups below 1024 units and
+# four-wave workgroups from 1024 on (LDS sized by the workgroup); both sides of
+# that switch, every unit compared, for both fixed pooling grids.
+@pytest.mark.parametrize("units,heads,d,m,dtype",
+                         [(1020, 6, 30, 16, "f32"), (1026, 6, 30, 16, "f32"),
+                          (1023, 1, 32, 8, "bf16"), (1025, 1, 32, 8, "bf16")])
+def test_small_kernel_launch_geometry(units, heads, d, m, dtype):
+    assert units % heads == 0
+    shape = (units // heads, heads, 64, d)
+    assert B.nystra_select_variant(64, d, m, B.F32 if dtype == "f32" else B.BF16) == B.VARIANT_TILED
+    q, k, v = W.iid(shape, seed=units + d, dtype=dtype)
+    ref = oracle.forward(q, k, v, m, iters=6, mode=0)
+    got = run(q, k, v, m, dtype, B.VARIANT_TILED)
+    check_config(got, ref, dtype, f"{units} units {dtype}")
