@@ -73,15 +73,14 @@ __device__ inline void write_tile(float *B, int a, int b, f4 v, int g, int c)
 template <int M, int PB>
 __device__ inline void publish_bf(uint16_t *reg, int a, int b, f4 v, int g, int c)
 {
+    // Pairs converted together (round to nearest even), the hi terms widened
+    // back by a shift or a mask: the values of an element-wise split.
     uint32_t h[2], l[2];
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
-        const __bf16 h0 = (__bf16)v[2 * p], h1 = (__bf16)v[2 * p + 1];
-        const __bf16 l0 = (__bf16)(v[2 * p] - (float)h0), l1 = (__bf16)(v[2 * p + 1] - (float)h1);
-        h[p] = uint32_t(__builtin_bit_cast(uint16_t, h0)) |
-               (uint32_t(__builtin_bit_cast(uint16_t, h1)) << 16);
-        l[p] = uint32_t(__builtin_bit_cast(uint16_t, l0)) |
-               (uint32_t(__builtin_bit_cast(uint16_t, l1)) << 16);
+        h[p] = cvt_bf16x2(v[2 * p], v[2 * p + 1]);
+        const float h0 = __uint_as_float(h[p] << 16), h1 = __uint_as_float(h[p] & 0xffff0000u);
+        l[p] = cvt_bf16x2(v[2 * p] - h0, v[2 * p + 1] - h1);
     }
     uint16_t *hp = reg + (16 * b + c) * PB + 16 * a + 4 * g;
     *reinterpret_cast<uint2 *>(hp) = make_uint2(h[0], h[1]);
