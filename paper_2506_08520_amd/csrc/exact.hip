@@ -104,10 +104,9 @@ __device__ inline U16B load_chunk8_raw(const uint16_t *row, int g)
 
 __device__ inline bf8 as_bf8(const U16B &u) { return __builtin_bit_cast(bf8, u); }
 
-__device__ inline uint32_t pack_bf16(float lo, float hi)
-{
-    return uint32_t(f32_to_bf16(lo)) | (uint32_t(f32_to_bf16(hi)) << 16);
-}
+// Two probabilities (finite, in [0, 1]) as a bf16 pair, rounded to nearest
+// even by the conversion instruction.
+__device__ inline uint32_t pack_bf16(float lo, float hi) { return cvt_bf16x2(lo, hi); }
 
 constexpr int kExactWaves = 4;
 
