@@ -129,22 +129,25 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     const uint16_t *vu16 = reinterpret_cast<const uint16_t *>(vu);
     // Key groups are software-pipelined: the loads of group t0 + kGroup are
     // issued before group t0 is computed (past the end they repeat the last
-    // tile and go unused).  Chunks are loaded raw and their overlapping slots
-    // zeroed when the group is consumed, so no instruction waits on a load
-    // at its issue.
+    // tile and go unused).  Chunks are loaded raw, so no instruction waits on
+    // a load at its issue.
+    // bf16 V is held as pairs of rows (4g, 4g+1) and (4g+2, 4g+3) of one
+    // column, the two 16-bit loads landing in the halves of one register.
+    typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
     float kr[kGroup][8], vr[kGroup][2][4], krn[kGroup][8], vrn[kGroup][2][4];
     bf8 kw[kGroup], kwn[kGroup];
-    uint16_t vh[kGroup][2][4], vhn[kGroup][2][4];
+    uint32_t vh[kGroup][2][2], vhn[kGroup][2][2];
     auto load_group = [&](int t0, float (&kr_)[kGroup][8], bf8 (&kw_)[kGroup],
-                          float (&vr_)[kGroup][2][4], uint16_t (&vh_)[kGroup][2][4]) {
+                          float (&vr_)[kGroup][2][4], uint32_t (&vh_)[kGroup][2][2]) {
 #pragma unroll
         for (int u = 0; u < kGroup; ++u) {
+            // 32-bit offsets from the unit's (uniform) base: N d < 2^26
             const int tt = min(t0 + u, NT - 1);
-            const int64_t row = int64_t(16 * tt + c) * d;
+            const unsigned row = unsigned(16 * tt + c) * d;
             if constexpr (BFM)
-                kw_[u] = load_row8_bf16(ku16 + row + chunk_start<D>(g));
+                kw_[u] = load_row8_bf16(ku16 + (row + chunk_start<D>(g)));
             else if constexpr (E::bytes == 4)
-                load_row8<D>(ku + row + chunk_start<D>(g), kr_[u]);
+                load_row8<D>(ku + (row + chunk_start<D>(g)), kr_[u]);
             else   // bf16 values through the fp32 path: unpacked (and masked) here
                 load_chunk8<E, D>(ku + row, g, kr_[u]);
 #pragma unroll
@@ -152,30 +155,31 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                 const int f = 16 * ct + c;
                 // Columns past d repeat column d - 1: they reach only columns
                 // of T, W and O that are never stored (T_D is summed apart).
-                const int64_t vrow = int64_t(16 * tt + 4 * g) * d + min(f, d - 1);
+                // one address per row group; the four rows are immediate offsets
+                const unsigned vrow = unsigned(16 * tt + 4 * g) * d + unsigned(min(f, d - 1));
+                const uint16_t *vp16 = vu16 + vrow;
+                const typename E::T *vp = vu + vrow;
+                if constexpr (BFM) {
 #pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    if constexpr (BFM)
-                        vh_[u][ct][s] = vu16[vrow + s * d];
-                    else
-                        vr_[u][ct][s] = E::load(vu, vrow + s * d);
+                    for (int p = 0; p < 2; ++p) {
+                        u16x2 pr;
+                        pr.x = vp16[2 * p * d];
+                        pr.y = vp16[(2 * p + 1) * d];
+                        vh_[u][ct][p] = __builtin_bit_cast(uint32_t, pr);
+                    }
+                } else {
+#pragma unroll
+                    for (int s = 0; s < 4; ++s)
+                        vr_[u][ct][s] = E::load(vp, s * d);
                 }
             }
         }
     };
-    load_group(0, kr, kw, vr, vh);
-    for (int t0 = 0; t0 < NT; t0 += kGroup) {
-        load_group(t0 + kGroup, krn, kwn, vrn, vhn);
-#pragma unroll
-        for (int u = 0; u < kGroup; ++u) {
-            if constexpr (BFM) {
-                kw[u] = mask_chunk8_bf8<D>(kw[u], g);
-            } else {
-#pragma unroll
-                for (int s = 0; s < 8; ++s)
-                    kr[u][s] = slot_valid<D>(g, s) ? kr[u][s] : 0.f;
-            }
-        }
+    // One group of key tiles: masks, logits, running maxima, G_U^n and T.
+    // The K chunks stay unmasked: their overlapping slots meet zeros in the
+    // Qbar slots (Step 1 zeroes them).
+    auto process = [&](int t0, float (&kr)[kGroup][8], bf8 (&kw)[kGroup],
+                       float (&vr)[kGroup][2][4], uint32_t (&vh)[kGroup][2][2]) {
         // Logits of the group (a repeated last tile leaves the maximum unchanged
         // and is not accumulated).
         f4 su[kGroup];
@@ -218,8 +222,7 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                     U16B vb;
 #pragma unroll
                     for (int j = 0; j < 4; ++j)
-                        vb.w[j] = uint32_t(vh[u + (j >> 1)][ct][2 * (j & 1)]) |
-                                  (uint32_t(vh[u + (j >> 1)][ct][2 * (j & 1) + 1]) << 16);
+                        vb.w[j] = vh[u + (j >> 1)][ct][j & 1];
                     const bf8 vv = __builtin_bit_cast(bf8, vb);
                     T[ct] = mfma_bf16(gh, vv, T[ct]);
                     T[ct] = mfma_bf16(gl, vv, T[ct]);
@@ -243,20 +246,16 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                         T[ct] = mfma4(e[s], vr[u][ct][s], T[ct]);
             }
         }
-#pragma unroll
-        for (int u = 0; u < kGroup; ++u) {
-            kw[u] = kwn[u];
-#pragma unroll
-            for (int x = 0; x < 8; ++x)
-                kr[u][x] = krn[u][x];
-#pragma unroll
-            for (int ct = 0; ct < 2; ++ct)
-#pragma unroll
-                for (int x = 0; x < 4; ++x) {
-                    vr[u][ct][x] = vrn[u][ct][x];
-                    vh[u][ct][x] = vhn[u][ct][x];
-                }
-        }
+    };
+    // Unrolled by two with two buffers, so that no loaded row is copied.
+    load_group(0, kr, kw, vr, vh);
+    for (int t0 = 0; t0 < NT; t0 += 2 * kGroup) {
+        load_group(t0 + kGroup, krn, kwn, vrn, vhn);
+        process(t0, kr, kw, vr, vh);
+        if (t0 + kGroup >= NT)
+            break;   // uniform
+        load_group(t0 + 2 * kGroup, kr, kw, vr, vh);
+        process(t0 + kGroup, krn, kwn, vrn, vhn);
     }
     const float mu = a.s2 * mrun;   // m_U of landmark l (base-2 units)
     tden = sum_groups(tden);   // T_D of landmark l
