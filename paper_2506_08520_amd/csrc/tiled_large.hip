@@ -45,6 +45,9 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 {
     using L = LargeLds<MT>;
     constexpr int d = D;
+    // With a spare column (D % 16 != 0), column D of V is replaced by ones, so
+    // that column D of T, W and O carries T_D, W_D and O_D (no separate sums).
+    constexpr bool PAD = D % 16 != 0;
     extern __shared__ float lds[];
     float *kbar = lds + L::kbar;
 
@@ -180,6 +183,21 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     // Qbar slots (Step 1 zeroes them).
     auto process = [&](int t0, float (&kr)[kGroup][8], bf8 (&kw)[kGroup],
                        float (&vr)[kGroup][2][4], uint32_t (&vh)[kGroup][2][2]) {
+        if constexpr (PAD) {
+            const bool ones = c == D % 16;   // column D, in feature tile D / 16
+#pragma unroll
+            for (int u = 0; u < kGroup; ++u) {
+                if constexpr (BFM) {
+#pragma unroll
+                    for (int p = 0; p < 2; ++p)
+                        vh[u][D / 16][p] = ones ? 0x3F803F80u : vh[u][D / 16][p];   // bf16 1.0, twice
+                } else {
+#pragma unroll
+                    for (int x = 0; x < 4; ++x)
+                        vr[u][D / 16][x] = ones ? 1.f : vr[u][D / 16][x];
+                }
+            }
+        }
         // Logits of the group (a repeated last tile leaves the maximum unchanged
         // and is not accumulated).
         f4 su[kGroup];
@@ -213,7 +231,8 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
                         gk[4 * h + i] = lval ? fast_exp2(fmaf(a.s2, su[u + h][i], -mb)) : 0.f;
-                        tden += gk[4 * h + i];
+                        if constexpr (!PAD)
+                            tden += gk[4 * h + i];
                     }
                 bf8 gh, gl;
                 split_bf16(gk, gh, gl);
@@ -237,7 +256,8 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     e[i] = lval ? fast_exp2(fmaf(a.s2, su[u][i], -mb)) : 0.f;
-                    tden += e[i];
+                    if constexpr (!PAD)
+                        tden += e[i];
                 }
 #pragma unroll
                 for (int ct = 0; ct < 2; ++ct)
@@ -258,7 +278,10 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         process(t0 + kGroup, krn, kwn, vrn, vhn);
     }
     const float mu = a.s2 * mrun;   // m_U of landmark l (base-2 units)
-    tden = sum_groups(tden);   // T_D of landmark l
+    // T_D of landmark l (with the ones column it is column D of T, and the
+    // core's separate W_D goes unused)
+    if constexpr (!PAD)
+        tden = sum_groups(tden);
     __syncthreads();           // Kbar complete
 
     landmark_core<MT, D, BFM, FULL>(lds, qb, mu, T, tden, m, a.iters, a.s2, lt, lane);
@@ -355,14 +378,17 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                     const float e = (FULL || 16 * kk + 4 * g + i < m)
                                         ? fast_exp2(fmaf(a.s2, glT[kk][i], -ml)) : 0.f;
                     glT[kk][i] = e;
-                    od = fmaf(e, wdv[kk][i], od);
+                    if constexpr (!PAD)
+                        od = fmaf(e, wdv[kk][i], od);
                 }
-            od = sum_groups(od);
-            const f4 odr = by_rows(od, vec, g, c);   // O_D[16tt + 4g + i]
-            f4 rcp;
+            f4 rcp;   // 1 / O_D[16tt + 4g + i]
+            if constexpr (!PAD) {
+                od = sum_groups(od);
+                const f4 odr = by_rows(od, vec, g, c);
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                rcp[i] = __builtin_amdgcn_rcpf(odr[i]);
+                for (int i = 0; i < 4; ++i)
+                    rcp[i] = __builtin_amdgcn_rcpf(odr[i]);
+            }
             bf8 gh[MP], gl[MP];
             if constexpr (BFM) {
 #pragma unroll
@@ -376,6 +402,7 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                     split_bf16(g8, gh[kp], gl[kp]);
                 }
             }
+            f4 ont[2];
 #pragma unroll
             for (int ct = 0; ct < 2; ++ct) {
                 f4 on = {0.f, 0.f, 0.f, 0.f};
@@ -391,6 +418,17 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                     for (int kk = 0; kk < MT; ++kk)
                         on = mm16_acc(glT[kk], WR[kk][ct], on);
                 }
+                ont[ct] = on;
+            }
+            if constexpr (PAD) {
+                // O_D is column D: lane D % 16 of each row of feature tile D / 16
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    rcp[i] = __builtin_amdgcn_rcpf(row_bcast<D % 16>(ont[D / 16][i]));
+            }
+#pragma unroll
+            for (int ct = 0; ct < 2; ++ct) {
+                const f4 on = ont[ct];
                 const int f = 16 * ct + c;
                 if (f < d) {
                     const int64_t orow = int64_t(16 * tt + 4 * g) * d + f;
