@@ -62,7 +62,7 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     typename E::T *ou = o + base;
 
     // ---- Step 1: means of this landmark's patch (rows r0.., cols c0..),
-    // four patch tokens per step so their loads are in flight together.
+    // eight patch tokens per step so their loads are in flight together.
     float qb[8], kbv[8];
 #pragma unroll
     for (int s = 0; s < 8; ++s)
@@ -71,30 +71,50 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         const int le = lval ? l : m - 1;   // padding lanes read a valid patch, then drop it
         const int r0 = (le / a.gc) * a.pr, c0 = (le % a.gc) * a.pc;
         const int npatch = a.pr * a.pc;
-        for (int j0 = 0; j0 < npatch; j0 += 4) {
-            float x[4][8], y[4][8];
+        // Rows arrive raw; the slots a lower lane group carries are zeroed
+        // once, in the sums (the same values as zeroing every row).
+        constexpr int kP = 8;
+        for (int j0 = 0; j0 < npatch; j0 += kP) {
+            float x[kP][8], y[kP][8];   // fp32 rows
+            U16B xb[kP], yb[kP];        // bf16 rows (raw pairs)
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u = 0; u < kP; ++u) {
                 const int j = min(j0 + u, npatch - 1);
-                const int64_t t = int64_t(r0 + j / a.pc) * a.cols + c0 + j % a.pc;
-                load_chunk8<E, D>(qu + t * d, g, x[u]);
-                load_chunk8<E, D>(ku + t * d, g, y[u]);
+                const int64_t t = (int64_t(r0 + j / a.pc) * a.cols + c0 + j % a.pc) * d +
+                                  chunk_start<D>(g);
+                if constexpr (E::bytes == 4) {
+                    load_row8<D>(qu + t, x[u]);
+                    load_row8<D>(ku + t, y[u]);
+                } else {
+                    xb[u] = *reinterpret_cast<const U16B *>(qu + t);
+                    yb[u] = *reinterpret_cast<const U16B *>(ku + t);
+                }
             }
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
+            for (int u = 0; u < kP; ++u)
                 if (j0 + u < npatch) {
+                    if constexpr (E::bytes == 4) {
 #pragma unroll
-                    for (int s = 0; s < 8; ++s) {
-                        qb[s] += x[u][s];
-                        kbv[s] += y[u][s];
+                        for (int s = 0; s < 8; ++s) {
+                            qb[s] += x[u][s];
+                            kbv[s] += y[u][s];
+                        }
+                    } else {
+#pragma unroll
+                        for (int w = 0; w < 4; ++w) {
+                            qb[2 * w] += __uint_as_float(xb[u].w[w] << 16);
+                            qb[2 * w + 1] += __uint_as_float(xb[u].w[w] & 0xffff0000u);
+                            kbv[2 * w] += __uint_as_float(yb[u].w[w] << 16);
+                            kbv[2 * w + 1] += __uint_as_float(yb[u].w[w] & 0xffff0000u);
+                        }
                     }
                 }
         }
         const float sc = lval ? a.inv_patch : 0.f;
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
-            qb[s] *= sc;
-            kbv[s] *= sc;
+            qb[s] = slot_valid<D>(g, s) ? qb[s] * sc : 0.f;
+            kbv[s] = slot_valid<D>(g, s) ? kbv[s] * sc : 0.f;
         }
     }
 #pragma unroll
