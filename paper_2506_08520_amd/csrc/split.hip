@@ -217,14 +217,17 @@ split_keys_kernel(const typename E::T *__restrict__ k, const typename E::T *__re
     // is not accumulated.
     // The pairs are software-pipelined: the next pair's K and V rows are
     // requested before this pair is computed (past the end they repeat the
-    // last tile, unused).  Rows arrive raw; masks and the ones column are
-    // applied when the pair is consumed, so no instruction waits on a load at
-    // its issue.
+    // last tile, unused).  Rows arrive raw and the ones column is applied
+    // when the pair is consumed, so no instruction waits on a load at its
+    // issue.
+    // bf16 V is held as pairs of rows (4g, 4g+1) and (4g+2, 4g+3) of one
+    // column, the two 16-bit loads landing in the halves of one register.
+    typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
     float kr[2][8], vr[2][NCT][4], krn[2][8], vrn[2][NCT][4];
     bf8 kw[2], kwn[2];
-    uint16_t vh[2][NCT][4], vhn[2][NCT][4];
+    uint32_t vh[2][NCT][2], vhn[2][NCT][2];
     auto load_pair = [&](int t0, float (&kr_)[2][8], bf8 (&kw_)[2], float (&vr_)[2][NCT][4],
-                         uint16_t (&vh_)[2][NCT][4]) {
+                         uint32_t (&vh_)[2][NCT][2]) {
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
             const int tt = min(t0 + u, NT - 1);
@@ -239,37 +242,42 @@ split_keys_kernel(const typename E::T *__restrict__ k, const typename E::T *__re
             for (int ct = 0; ct < NCT; ++ct) {
                 const int f = 16 * ct + c;
                 const int64_t vrow = int64_t(k0 + 16 * tt + 4 * g) * d + min(f, d - 1);
+                const uint16_t *vp16 = vu16 + vrow;   // the four rows: immediate offsets
+                const typename E::T *vp = vu + vrow;
+                if constexpr (BFM) {
 #pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    if constexpr (BFM)
-                        vh_[u][ct][s] = vu16[vrow + s * d];
-                    else
-                        vr_[u][ct][s] = E::load(vu, vrow + s * d);
+                    for (int pp = 0; pp < 2; ++pp) {
+                        u16x2 pr;
+                        pr.x = vp16[2 * pp * d];
+                        pr.y = vp16[(2 * pp + 1) * d];
+                        vh_[u][ct][pp] = __builtin_bit_cast(uint32_t, pr);
+                    }
+                } else {
+#pragma unroll
+                    for (int s = 0; s < 4; ++s)
+                        vr_[u][ct][s] = E::load(vp, s * d);
                 }
             }
         }
     };
-    load_pair(2 * w, kr, kw, vr, vh);
-    for (int t0 = 2 * w; t0 < NT; t0 += 2 * kWaves) {
-        load_pair(t0 + 2 * kWaves, krn, kwn, vrn, vhn);
+    // One pair of key tiles: ones column, logits, running maxima, G_U^n and T.
+    auto process = [&](int t0, float (&kr)[2][8], bf8 (&kw)[2], float (&vr)[2][NCT][4],
+                       uint32_t (&vh)[2][NCT][2]) {
+        // The K chunks stay unmasked (their overlapping slots meet zeros in the
+        // Qbar slots); V columns past d become the ones column, then zeros.
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-            if constexpr (BFM) {
-                kw[u] = mask_chunk8_bf8<D>(kw[u], g);
-            } else if constexpr (E::bytes == 4) {
-#pragma unroll
-                for (int s = 0; s < 8; ++s)
-                    kr[u][s] = slot_valid<D>(g, s) ? kr[u][s] : 0.f;
-            }
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) {
                 const int f = 16 * ct + c;
+                if constexpr (BFM) {
 #pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    if constexpr (BFM)
-                        vh[u][ct][s] = f < d ? vh[u][ct][s]
-                                             : uint16_t(kOnes && f == d ? 0x3F80u : 0u);
-                    else
+                    for (int pp = 0; pp < 2; ++pp)
+                        vh[u][ct][pp] = f < d ? vh[u][ct][pp]
+                                              : (kOnes && f == d ? 0x3F803F80u : 0u);
+                } else {
+#pragma unroll
+                    for (int s = 0; s < 4; ++s)
                         vr[u][ct][s] = f < d ? vr[u][ct][s] : (kOnes && f == d ? 1.f : 0.f);
                 }
             }
@@ -282,8 +290,7 @@ split_keys_kernel(const typename E::T *__restrict__ k, const typename E::T *__re
                 U16B vb;
 #pragma unroll
                 for (int jj = 0; jj < 4; ++jj)
-                    vb.w[jj] = uint32_t(vh[jj >> 1][ct][2 * (jj & 1)]) |
-                               (uint32_t(vh[jj >> 1][ct][2 * (jj & 1) + 1]) << 16);
+                    vb.w[jj] = vh[jj >> 1][ct][jj & 1];
                 vv[ct] = __builtin_bit_cast(bf8, vb);
             }
         }
@@ -358,19 +365,34 @@ split_keys_kernel(const typename E::T *__restrict__ k, const typename E::T *__re
                 }
             }
         }
+    };
+    // Unrolled by two with two buffers, so that no loaded row is copied --
+    // except for bf16 with three or four landmark tiles, where the unrolled
+    // loop needs more registers than three waves per SIMD leave (measured
+    // slower there).
+    load_pair(2 * w, kr, kw, vr, vh);
+    if constexpr (!(BFM && MT >= 3)) {
+        for (int t0 = 2 * w; t0 < NT; t0 += 4 * kWaves) {
+            load_pair(t0 + 2 * kWaves, krn, kwn, vrn, vhn);
+            process(t0, kr, kw, vr, vh);
+            if (t0 + 2 * kWaves >= NT)
+                break;   // uniform
+            load_pair(t0 + 4 * kWaves, kr, kw, vr, vh);
+            process(t0 + 2 * kWaves, krn, kwn, vrn, vhn);
+        }
+    } else {
+        for (int t0 = 2 * w; t0 < NT; t0 += 2 * kWaves) {
+            load_pair(t0 + 2 * kWaves, krn, kwn, vrn, vhn);
+            process(t0, kr, kw, vr, vh);
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            kw[u] = kwn[u];
+            for (int u = 0; u < 2; ++u) {
+                kw[u] = kwn[u];
 #pragma unroll
-            for (int x = 0; x < 8; ++x)
-                kr[u][x] = krn[u][x];
+                for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-            for (int ct = 0; ct < NCT; ++ct)
-#pragma unroll
-                for (int x = 0; x < 4; ++x) {
-                    vr[u][ct][x] = vrn[u][ct][x];
-                    vh[u][ct][x] = vhn[u][ct][x];
-                }
+                    for (int x = 0; x < 2; ++x)
+                        vh[u][ct][x] = vhn[u][ct][x];
+            }
         }
     }
 
