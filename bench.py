@@ -292,7 +292,8 @@ def block_bench(args):
 
     def timed(fn, reps):
         s = torch.cuda.current_stream()
-        fn()
+        for _ in range(max(3, reps // 2)):   # warm-up: clocks, caches, first-call costs
+            fn()
         r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         r0.record(s)
