@@ -4,10 +4,13 @@ One step = one PnP-Nystra forward (landmark pooling, kernel blocks,
 pseudo-inverse, value products, normalisation -- the whole path, one fused
 launch) over the SwinIR-like layer: a 256x256x180 feature map in 8x8 windows,
 1024 windows x 6 heads, N = 64, d_h = 30, m = 16 landmarks, K = 6
-pseudo-inverse iterations, fp32 storage (a bf16 run of the same layer is
-reported alongside).  Inputs are synthetic (seeded) and resident in HBM; the
-steps rotate over enough copies of them (> 1 GiB) that no step is served from
-the 256 MB Infinity Cache.
+pseudo-inverse iterations, fp32 storage.  Every other workload (the 8x8,
+16x16 and 32x32 window configurations in each storage type they are run in)
+is timed the same way and reported in "configs": kernel time, tokens/s, HBM
+and matrix-core fractions of the MI355X peaks, and exact attention on the
+same buffers with its own distance from its floor.  Inputs are synthetic
+(seeded) and resident in HBM; the steps rotate over enough copies of them
+(> 1 GiB) that no step is served from the 256 MB Infinity Cache.
 
 Prints ONE JSON line (rank 0, N = 1 GPU).
 """
@@ -23,6 +26,12 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E peak, GB/s
+# Dense matrix-core peaks by storage type (fp32 inputs run the fp32 matrix
+# cores, bf16 inputs the bf16 ones), TFLOP/s.
+MFMA_PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
+# v_exp_f32 per second: a quarter of the unpacked fp32 lane rate
+# (157.3 TFLOP/s = 2 flops x 2 packed lanes x 39.3 T lane-ops/s).
+EXP_PEAK_PER_S = 157.3e12 / 4 / 4
 ROTATE_BYTES = 1.2 * (1 << 30)  # working set cycled by the timed steps
 
 
@@ -38,10 +47,14 @@ def parse():
     ap.add_argument("--dtype", default="f32", choices=["f32", "bf16"])
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-exact", action="store_true", help="skip the exact-attention timing")
-    ap.add_argument("--no-alt", action="store_true", help="skip the other-dtype run")
+    ap.add_argument("--no-alt", action="store_true",
+                    help="time only the headline workload (--config, --dtype)")
+    ap.add_argument("--configs", default=",".join(ALL_CASES),
+                    help="config:dtype pairs timed besides the headline, one record each")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the same-traffic elementwise kernel (the practical HBM ceiling)")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="wall-clock budget of each CPU-baseline leg (all threads, one thread)")
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the benchmark line: time PnP-Nystra and exact attention "
                          "over N x m x K on the smooth-field recipe and report the error "
@@ -83,10 +96,10 @@ def time_kernel(case, launch, steps, warmup, preheat=0.0):
 
     Returns (ms per step by the host clock between the synchronisations that
     bracket the timed launches, ms per launch from one HIP event pair around
-    the same launches, and -- as a diagnostic only -- the mean of event pairs
-    recorded around each launch of a second pass, which also counts the
-    events' own overhead).  All events are recorded on the stream the
-    kernels are launched on."""
+    the same launches, and -- as a diagnostic only -- the 10th, 50th and 90th
+    percentiles of event pairs recorded around each launch of a second pass,
+    which also count the events' own overhead).  All events are recorded on
+    the stream the kernels are launched on."""
     import torch
     stream = torch.cuda.current_stream()
     # The first launches after idle run at lower clocks (c2 fp32: 51.7 us
@@ -110,7 +123,7 @@ def time_kernel(case, launch, steps, warmup, preheat=0.0):
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     region = r0.elapsed_time(r1) / steps
-    n = min(steps, 20)
+    n = min(steps, 50)
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
     stops = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
     for i in range(n):
@@ -118,8 +131,9 @@ def time_kernel(case, launch, steps, warmup, preheat=0.0):
         launch(*case.sets[(warmup + steps + i) % case.nsets], stream)
         stops[i].record(stream)
     torch.cuda.synchronize()
-    pairs = sum(a.elapsed_time(b) for a, b in zip(starts, stops)) / n
-    return (t1 - t0) * 1e3 / steps, region, pairs, heat
+    each = sorted(a.elapsed_time(b) for a, b in zip(starts, stops))
+    pct = [each[min(n - 1, int(round(f * (n - 1))))] for f in (0.1, 0.5, 0.9)]
+    return (t1 - t0) * 1e3 / steps, region, pct, heat
 
 
 def measured_traffic(cfg, dtype, variant):
@@ -141,10 +155,11 @@ def measured_traffic(cfg, dtype, variant):
     return rec["fetch_bytes"] + rec["write_bytes"]
 
 
-def cpu_baseline(wl, q, k, v, budget_s):
+def cpu_baseline(wl, q, k, v, budget_s, n_threads=0):
     """The float64 oracle on a bounded sample of the same units: a strided
     subset when the whole workload would overrun the budget, otherwise the
-    whole workload repeated until the budget is spent."""
+    whole workload repeated until the budget is spent.  n_threads = 0 runs
+    OpenMP's default thread count (all cores given to the process)."""
     import numpy as np
     import oracle
     units = wl.units
@@ -152,27 +167,32 @@ def cpu_baseline(wl, q, k, v, budget_s):
     probe = min(units, 48)
     idx = np.linspace(0, units - 1, probe).round().astype(np.int64)
     t0 = time.perf_counter()
-    oracle.forward(*(x[idx] for x in flat), wl.m)
+    oracle.forward(*(x[idx] for x in flat), wl.m, n_threads=n_threads)
     t_probe = time.perf_counter() - t0
     per_unit = max(t_probe, 1e-6) / probe
     n = int(min(units, max(probe, budget_s / per_unit)))
     idx = np.linspace(0, units - 1, n).round().astype(np.int64)
     sample = [np.ascontiguousarray(x[idx]) for x in flat]
-    reps = 0
+    passes = []
     t0 = time.perf_counter()
     while True:   # whole passes until the budget is spent (at least one)
-        oracle.forward(*sample, wl.m)
-        reps += 1
+        tp = time.perf_counter()
+        oracle.forward(*sample, wl.m, n_threads=n_threads)
+        passes.append(time.perf_counter() - tp)
         dt = time.perf_counter() - t0
         if dt >= budget_s or n < units:
             break
+    reps = len(passes)
     tokens = reps * n * wl.N / wl.heads   # spatial tokens (all heads) processed
     what = (f"all {units} units x {reps} passes" if n == units
             else f"{n} of {units} units, strided")
-    return {"value": tokens / dt, "unit": "tokens/s", "cores": oracle.max_threads(),
-            "kind": "oracle",
+    cores = oracle.max_threads() if n_threads <= 0 else n_threads
+    ps = sorted(passes)
+    pct = [ps[min(reps - 1, int(round(f * (reps - 1))))] for f in (0.1, 0.5, 0.9)]
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": cores,
+            "kind": "oracle", "pass_s_p10_p50_p90": pct,
             "sample": f"{what} of {wl.name} ({wl.N} tokens, m={wl.m}, K=6); float64 C "
-                      f"oracle, {dt:.1f} s wall"}
+                      f"oracle, {cores} thread(s), {dt:.1f} s wall"}
 
 
 def sweep(args):
@@ -366,6 +386,127 @@ def block_bench(args):
     return 0
 
 
+# The measured workloads: every (configuration, storage type) pair.
+ALL_CASES = ("c1:f32", "c2:f32", "c2:bf16", "c3:bf16", "c4:f32", "c4:bf16", "c5:bf16")
+
+
+def nystrom_flops(N, d, m, K):
+    """Algorithmic flops of one unit of Algorithm 1 as the kernels evaluate
+    it (Steps 5-6 re-associated): Step 1 pooling sums (2 N d), S_L and S_U
+    (4 N m d), S_A (2 m^2 d), the pseudo-inverse (8 K m^3: four m x m
+    products per iteration), T = G_U^n [V | 1] and [O_N | O_D] = G_L^n W
+    (4 N m (d + 1)), W = Z T (2 m^2 (d + 1)) and the division (N d)."""
+    return (2 * N * d + 4 * N * m * d + 2 * m * m * d + 8 * K * m ** 3 + 4 * N * m * (d + 1) +
+            2 * m * m * (d + 1) + N * d)
+
+
+def exact_flops(N, d):
+    """Exact attention, Eq. (1): S = Q K^T and P V, 4 N^2 d flops per unit."""
+    return 4 * N * N * d
+
+
+def floors(wl, dtype, flops, exps):
+    """Lower bounds (ms) of one launch on MI355X: HBM bytes at 8 TB/s, the
+    flops at the matrix-core peak of the storage type, the exponentials at
+    the transcendental rate."""
+    hbm = wl.io_bytes(dtype) / (HBM_PEAK_GBS * 1e9) * 1e3
+    mfma = wl.units * flops / (MFMA_PEAK_TFLOPS[dtype] * 1e12) * 1e3
+    exp = wl.units * exps / EXP_PEAK_PER_S * 1e3
+    return {"hbm": hbm, "mfma": mfma, "exp": exp}
+
+
+def measure(wl, dtype, args, q, k, v, headline):
+    """Times PnP-Nystra (and, unless disabled, exact attention and the
+    same-traffic elementwise kernel) on one workload; returns the record."""
+    import torch
+    from paper_2506_08520_amd import binding as B
+
+    case = Case(wl, dtype, q, k, v)
+
+    def nys(q_, k_, v_, o_, s):
+        B.nystra_attn_forward(q_, k_, v_, wl.m, out=o_, stream=s)
+
+    def ex(q_, k_, v_, o_, s):
+        B.nystra_exact_attn_forward(q_, k_, v_, out=o_, stream=s)
+
+    steps = args.steps
+    ms, kern, pairs, heat = time_kernel(case, nys, steps, args.warmup, args.preheat)
+    code = B.F32 if dtype == "f32" else B.BF16
+    K = 6
+    fl = nystrom_flops(wl.N, wl.d, wl.m, K)
+    fl_floor = floors(wl, dtype, fl, 2 * wl.N * wl.m + wl.m * wl.m)
+    floor_ms = max(fl_floor["hbm"], fl_floor["mfma"])
+    gbs = case.io_bytes / (kern * 1e-3) / 1e9
+    tfl = wl.units * fl / (kern * 1e-3) / 1e12
+    r = {
+        "config": wl.name, "storage": dtype, "n_windows": wl.n_windows, "heads": wl.heads,
+        "N": wl.N, "d_h": wl.d, "m": wl.m, "K": K,
+        "variant": {B.VARIANT_GENERIC: "generic", B.VARIANT_TILED: "mfma-tiled"}.get(
+            B.nystra_select_variant(wl.N, wl.d, wl.m, code), "?"),
+        "kernel_ms": kern, "ms_per_step": ms,
+        "kernel_ms_p10_p50_p90": [float(x) for x in pairs],
+        "tokens_per_s": wl.n_windows * wl.N / (kern * 1e-3),
+        "unit_tokens_per_s": wl.units * wl.N / (kern * 1e-3),
+        "hbm": {"algorithmic_bytes": case.io_bytes, "achieved_GBs": gbs,
+                "frac": gbs / HBM_PEAK_GBS},
+        "flops": {"per_unit": fl, "achieved_TFLOPs": tfl,
+                  "peak_TFLOPs": MFMA_PEAK_TFLOPS[dtype],
+                  "frac": tfl / MFMA_PEAK_TFLOPS[dtype]},
+        "bound": "hbm" if fl_floor["hbm"] >= fl_floor["mfma"] else "mfma",
+        "floor_ms": floor_ms, "roofline_frac": floor_ms / kern,
+        "preheat_launches": heat,
+    }
+    if not args.no_exact:
+        ems, ekern, epairs, _ = time_kernel(case, ex, max(10, steps // 4), args.warmup,
+                                            min(args.preheat, 0.3))
+        ef = floors(wl, dtype, exact_flops(wl.N, wl.d), wl.N * wl.N)
+        eb = max(ef, key=ef.get)
+        r["exact"] = {"kernel_ms": ekern, "ms_per_step": ems,
+                      "kernel_ms_p10_p50_p90": [float(x) for x in epairs],
+                      "floor_ms": ef[eb], "floor_bound": eb, "floors_ms": ef,
+                      "frac_of_floor": ef[eb] / ekern}
+        r["speedup_vs_exact"] = ekern / kern
+    if not args.no_ceiling and wl.N <= 64:
+        # The practical HBM ceiling for this traffic: one elementwise kernel
+        # that reads Q, K and V and writes O once (O = Q + K * V), on the
+        # same rotating buffers and stream -- the same bytes as one step,
+        # with no arithmetic to speak of.
+        def same_traffic(q_, k_, v_, o_, s):
+            torch.addcmul(q_, k_, v_, out=o_)
+
+        _, ckern, _, _ = time_kernel(case, same_traffic, steps, args.warmup,
+                                     min(args.preheat, 0.3))
+        cg = case.io_bytes / (ckern * 1e-3) / 1e9
+        r["same_traffic_ceiling"] = {
+            "kernel": "torch.addcmul: reads Q, K, V and writes O once, the bytes of one step",
+            "kernel_ms": ckern, "achieved_GBs": cg, "frac": cg / HBM_PEAK_GBS,
+            "nystrom_over_ceiling": gbs / cg}
+    if headline:
+        r["traffic"] = measured_traffic(wl.name, dtype, B.nystra_select_variant(
+            wl.N, wl.d, wl.m, code))
+    del case
+    torch.cuda.empty_cache()
+    return r
+
+
+def host_cpu():
+    """CPU model name and the number of cores this process may run on."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count()
+    return model, n
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -377,54 +518,33 @@ def main():
         return sweep(args)
     if args.block:
         return block_bench(args)
-    import torch
+    import torch  # noqa: F401
     from paper_2506_08520_amd import binding as B
     from paper_2506_08520_amd import workloads as W
 
     B.lib()
-    wl = W.CONFIGS[args.config]
-    dtypes = [args.dtype] + ([] if args.no_alt else [d for d in wl.dtypes if d != args.dtype])
-    results = {}
+    head = f"{args.config}:{args.dtype}"
+    cases = [head]
+    if not args.no_alt:
+        cases += [c for c in args.configs.split(",") if c and c != head]
+    records = {}
     main_inputs = None
-    for dt in dtypes:
+    for cd in cases:
+        cfg, dt = cd.split(":")
+        wl = W.CONFIGS[cfg]
         q, k, v = W.generate(wl, dt)
-        if dt == args.dtype:
+        if cd == head:
             main_inputs = (q, k, v)
-        case = Case(wl, dt, q, k, v)
+        records[cd] = measure(wl, dt, args, q, k, v, cd == head)
+        print(f"[bench] {cd}: {records[cd]['kernel_ms'] * 1e3:.1f} us"
+              + (f", exact {records[cd]['exact']['kernel_ms'] * 1e3:.1f} us"
+                 if "exact" in records[cd] else ""), file=sys.stderr, flush=True)
+        if cd != head:
+            del q, k, v
 
-        def nys(q_, k_, v_, o_, s):
-            B.nystra_attn_forward(q_, k_, v_, wl.m, out=o_, stream=s)
-
-        def ex(q_, k_, v_, o_, s):
-            B.nystra_exact_attn_forward(q_, k_, v_, out=o_, stream=s)
-
-        ms, kern, pairs, heat = time_kernel(case, nys, args.steps, args.warmup, args.preheat)
-        r = {"ms_per_step": ms, "kernel_ms": kern, "pairs_ms": pairs, "io_bytes": case.io_bytes,
-             "preheat_launches": heat,
-             "variant": B.nystra_select_variant(wl.N, wl.d, wl.m,
-                                                B.F32 if dt == "f32" else B.BF16)}
-        if not args.no_exact:
-            ems, ekern, _, _ = time_kernel(case, ex, max(10, args.steps // 4), args.warmup,
-                                           args.preheat)
-            r.update(exact_ms_per_step=ems, exact_kernel_ms=ekern)
-        if not args.no_ceiling:
-            # The practical HBM ceiling for this traffic: one elementwise kernel
-            # that reads Q, K and V and writes O once (O = Q + K * V), on the
-            # same rotating buffers and stream -- the same bytes as one step,
-            # with no arithmetic to speak of.
-            def same_traffic(q_, k_, v_, o_, s):
-                torch.addcmul(q_, k_, v_, out=o_)
-
-            _, ckern, _, _ = time_kernel(case, same_traffic, args.steps, args.warmup,
-                                         min(args.preheat, 0.3))
-            r["ceiling_kernel_ms"] = ckern
-        results[dt] = r
-        del case
-        torch.cuda.empty_cache()
-
-    r = results[args.dtype]
+    r = records[head]
+    wl = W.CONFIGS[args.config]
     tokens = wl.n_windows * wl.N
-    achieved = r["io_bytes"] / (r["kernel_ms"] * 1e-3) / 1e9
     line = {
         "metric": "Nystrom window-attention tokens/s at 1 MI355X; % peak HBM BW; "
                   "speedup vs exact",
@@ -439,41 +559,32 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": args.dtype,
         "data": "synthetic",
         "config": {"workload": f"{wl.name}: {wl.description}; {args.dtype} storage, "
                                "K=6 pseudo-inverse iterations, 2-D pooled landmarks",
                    "n_windows": wl.n_windows, "heads": wl.heads, "N": wl.N, "d_h": wl.d,
                    "m": wl.m, "storage": args.dtype},
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": measured_traffic(wl.name, args.dtype, r["variant"]),
-                     "algorithmic_bytes": r["io_bytes"]},
     }
-    if "exact_kernel_ms" in r:
-        line["speedup_vs_exact"] = r["exact_kernel_ms"] / r["kernel_ms"]
-    if "ceiling_kernel_ms" in r:
-        ceil_gbs = r["io_bytes"] / (r["ceiling_kernel_ms"] * 1e-3) / 1e9
-        line["same_traffic_ceiling"] = {
-            "kernel": "torch.addcmul: reads Q, K, V and writes O once, the bytes of one step",
-            "kernel_ms": r["ceiling_kernel_ms"], "achieved": ceil_gbs, "unit": "GB/s",
-            "frac": ceil_gbs / HBM_PEAK_GBS, "nystrom_over_ceiling": achieved / ceil_gbs}
+    if r["bound"] == "hbm":
+        line["roofline"] = {"bound": "hbm", "achieved": r["hbm"]["achieved_GBs"],
+                            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": r["hbm"]["frac"],
+                            "traffic": r["traffic"],
+                            "algorithmic_bytes": r["hbm"]["algorithmic_bytes"]}
+    else:
+        line["roofline"] = {"bound": "mfma", "achieved": r["flops"]["achieved_TFLOPs"],
+                            "peak": r["flops"]["peak_TFLOPs"], "unit": "TFLOP/s",
+                            "frac": r["flops"]["frac"], "traffic": r["traffic"],
+                            "algorithmic_flops": r["flops"]["per_unit"] * wl.units}
+    if "speedup_vs_exact" in r:
+        line["speedup_vs_exact"] = r["speedup_vs_exact"]
+    if "same_traffic_ceiling" in r:
+        line["same_traffic_ceiling"] = r["same_traffic_ceiling"]
     line["kernel_ms"] = r["kernel_ms"]
-    line["kernel_ms_event_pairs"] = r["pairs_ms"]
-    line["variant"] = "mfma-tiled" if r["variant"] == 2 else "generic"
-    for dt, rr in results.items():
-        if dt == args.dtype:
-            continue
-        ach = rr["io_bytes"] / (rr["kernel_ms"] * 1e-3) / 1e9
-        line[f"{dt}_storage"] = {
-            "value": tokens / (rr["ms_per_step"] * 1e-3), "ms_per_step": rr["ms_per_step"],
-            "kernel_ms": rr["kernel_ms"], "achieved_GBs": ach, "frac": ach / HBM_PEAK_GBS,
-            "speedup_vs_exact": (rr["exact_kernel_ms"] / rr["kernel_ms"]
-                                 if "exact_kernel_ms" in rr else None)}
-        if "ceiling_kernel_ms" in rr:
-            cg = rr["io_bytes"] / (rr["ceiling_kernel_ms"] * 1e-3) / 1e9
-            line[f"{dt}_storage"]["same_traffic_ceiling_frac"] = cg / HBM_PEAK_GBS
-            line[f"{dt}_storage"]["nystrom_over_ceiling"] = ach / cg
+    line["variant"] = r["variant"]
+    line["peaks"] = {"hbm_GBs": HBM_PEAK_GBS, "mfma_TFLOPs": MFMA_PEAK_TFLOPS,
+                     "exp_per_s": EXP_PEAK_PER_S}
+    line["configs"] = records
     if args.copy_mib > 0:
         n = args.copy_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -483,7 +594,14 @@ def main():
         torch.cuda.synchronize()
         line["copy_calibration_bytes"] = 2 * n * 4
     if not args.no_cpu:
-        line["cpu_baseline"] = cpu_baseline(wl, *main_inputs, args.cpu_seconds)
+        model, ncores = host_cpu()
+        cb = cpu_baseline(wl, *main_inputs, args.cpu_seconds, 0)
+        one = cpu_baseline(wl, *main_inputs, args.cpu_seconds, 1)
+        cb["host_cpu"] = model
+        cb["host_cores_available"] = ncores
+        cb["single_thread"] = {k_: one[k_] for k_ in ("value", "unit", "cores", "sample",
+                                                      "pass_s_p10_p50_p90")}
+        line["cpu_baseline"] = cb
     print(json.dumps(line), flush=True)
     return 0
 

@@ -15,7 +15,20 @@
  *   binary32, NYSTRA_BF16 = bfloat16).  Tokens of a window are row-major over
  *   its sqrt(N) x sqrt(N) pixel grid (SwinIR / Uformer window partition); the
  *   value width equals d_h.  O has the input dtype; bf16 outputs are rounded
- *   to nearest-even from an fp32 result.  All arithmetic is fp32.
+ *   to nearest-even from an fp32 result.
+ * Arithmetic.  fp32 inputs: fp32 throughout (fp32 matrix cores, fp32 VALU).
+ *   bf16 inputs: the stored bf16 values are exact operands; landmark means,
+ *   logits, row maxima, exponentials, sums and the Step 7 division are fp32.
+ *   The contractions of the MFMA-tiled and token-split kernels (S_L, S_U,
+ *   T = G_U^n [V | 1], O = G_L^n W and the Step 4 products) run on the bf16
+ *   matrix cores with fp32 accumulation, every fp32 operand carried as two
+ *   bf16 terms hi = bf16(x), lo = bf16(x - hi) (about 16 significant bits).
+ *   Where both factors are split, the 64-token kernel forms all four term
+ *   products; the larger-window and token-split kernels drop lo x lo (a
+ *   2^-16 relative term).  S_A and W = Z T stay fp32.  The resulting error
+ *   is ~1e-4 of the output RMS, far below the bf16 rounding of O.  The exact
+ *   kernel (nystra_exact_attn_forward) in bf16 rounds its probabilities to
+ *   bf16 for the P V product, as bf16 flash attention does (row sums fp32).
  * Streams.  `stream` is a hipStream_t (NULL = the null stream).  Work is
  *   enqueued and the call returns at once; the library never synchronises,
  *   allocates no device memory and keeps no mutable global state, so calls
@@ -26,11 +39,14 @@
  *   than NYSTRA_ERR_HIP no output is written.  n_windows == 0 or heads == 0
  *   is a valid no-op (pointers may then be NULL).  NYSTRA_ERR_HIP reports a
  *   failed launch; nystra_last_error() then holds the HIP message for the
- *   calling thread.  Nothing throws or aborts across this boundary.
+ *   calling thread.  Each entry point clears the thread's pending HIP error
+ *   (hipGetLastError) right before it launches, so an error left by an
+ *   earlier, unrelated HIP call is not reported as its own.  Nothing throws
+ *   or aborts across this boundary.
  * Limits.  1 <= N <= 2^20, 1 <= d_h <= 64, 1 <= m <= min(N, 64),
- *   n_windows * heads <= 2^31 - 1, 0 <= pinv_iters <= 64.  Pointers must be
- *   aligned to the element size.  O must not overlap Q, K or V (Q, K, V may
- *   alias each other).
+ *   n_windows * heads <= 2^24 - 1 (every grid stays under 2^32 work-items),
+ *   0 <= pinv_iters <= 64.  Pointers must be aligned to the element size.
+ *   O must not overlap Q, K or V (Q, K, V may alias each other).
  */
 #ifndef NYSTRA_H
 #define NYSTRA_H
@@ -167,7 +183,7 @@ int nystra_attn_forward_ws(const void *Q, const void *K, const void *V, void *O,
  * dtype stores them); products accumulate in fp32 on the matrix cores.
  * Limits: window divides height and width, 0 <= shift < window, heads
  * divides channels, d_h <= 64, channels <= 4096, batch * height * width
- * <= 2^31 - 1, and the attention limits above for N and m.
+ * <= 2^31 - 1, and the attention limits above for N, m and the unit count.
  * nystra_block_workspace_size: host-only size of the workspace
  * nystra_block_forward needs (Q, K, V, O and, for long windows, the
  * token-split workspace).  nystra_block_forward: workspace as for

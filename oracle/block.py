@@ -65,10 +65,13 @@ def round_bf16(x):
 
 
 def block_forward(x, w_qkv, b_qkv, w_proj, b_proj, heads, window, shift=0, m=16, iters=6,
-                  mode=0, attention="nystrom", dtype="f32", scale=None, n_threads=0):
+                  mode=0, attention="nystrom", dtype="f32", scale=None, n_threads=0,
+                  round_output=True):
     """y = block(x).  For dtype "bf16" every tensor the block stores (Q, K,
     V, the attention output, y) is rounded to bf16, as a bf16 model stores
-    them; arithmetic is float64 throughout."""
+    them; arithmetic is float64 throughout.  round_output=False leaves y
+    itself unrounded (the float64 value a bf16 store of y would round), so
+    that a comparison can tell y's own rounding from everything before it."""
     x = np.asarray(x, dtype=np.float64)
     B, H, W, C = x.shape
     d = C // heads
@@ -92,4 +95,5 @@ def block_forward(x, w_qkv, b_qkv, w_proj, b_proj, heads, window, shift=0, m=16,
     yw = ocat @ np.asarray(w_proj, np.float64) + np.asarray(b_proj, np.float64)
     y = np.empty((B * H * W, C))
     y[idx.reshape(-1)] = yw.reshape(-1, C)                     # windows back in place
-    return store(y.reshape(B, H, W, C))
+    y = y.reshape(B, H, W, C)
+    return store(y) if round_output else y

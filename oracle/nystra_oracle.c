@@ -390,11 +390,28 @@ int oracle_unit_trace(const double *Q, const double *K, const double *V, double 
     return rc;
 }
 
+/* Frobenius norm of the Step 4 residual I - A Z (A, Z: m x m, row-major). */
+/* Parity: pinned by the residual recurrence E_{k+1} = 3/4 E_k^3 + 1/4 E_k^4 */
+/* run from E_0 = I - A Z_0 (a derivation from the update, not the update).  */
+static double residual_fro(const double *A, const double *Z, int m)
+{
+    double acc = 0.0;
+    for (int i = 0; i < m; ++i)
+        for (int j = 0; j < m; ++j) {
+            double x = (i == j) ? 1.0 : 0.0;
+            for (int q = 0; q < m; ++q)
+                x -= A[i * m + q] * Z[q * m + j];
+            acc += x * x;
+        }
+    return sqrt(acc);
+}
+
 /* ------------------------------------------------------------------------ */
 /* Batched forward over `units` independent (window, head) units laid out    */
-/* contiguously as [units][N][d].  diag (optional, units x 2) receives the   */
-/* minimum and maximum of O_D per unit.  n_threads <= 0 uses the OpenMP      */
-/* default.  Returns the first nonzero status of any unit.                    */
+/* contiguously as [units][N][d].  diag (optional, units x 3) receives per    */
+/* unit the minimum and maximum of O_D and the Frobenius norm of the Step 4   */
+/* residual I - G_A^n Z_K.  n_threads <= 0 uses the OpenMP default.  Returns  */
+/* the first nonzero status of any unit.                                      */
 /* ------------------------------------------------------------------------ */
 int oracle_forward(const double *Q, const double *K, const double *V, double *O,
                    long units, int N, int d, int m, int iters, int mode, double scale,
@@ -444,8 +461,9 @@ int oracle_forward(const double *Q, const double *K, const double *V, double *O,
                     if (b.OD[i] > hi)
                         hi = b.OD[i];
                 }
-                diag[2 * u] = lo;
-                diag[2 * u + 1] = hi;
+                diag[3 * u] = lo;
+                diag[3 * u + 1] = hi;
+                diag[3 * u + 2] = residual_fro(b.GA, b.Z, m);
             }
         }
         unit_free(&b);

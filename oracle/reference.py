@@ -112,7 +112,10 @@ def unit_trace(Q, K, V, m, iters=6, mode=0, scale=None):
 
 
 def forward(Q, K, V, m, iters=6, mode=0, scale=None, n_threads=0, diag=False):
-    """Batched PnP-Nystra over [..., N, d] inputs (all leading dims are units)."""
+    """Batched PnP-Nystra over [..., N, d] inputs (all leading dims are units).
+
+    With diag, also returns per unit (units x 3): min O_D, max O_D (Step 7's
+    denominators) and ||I - G_A^n Z_K||_F (the Step 4 residual)."""
     Q, K, V = _f64(Q), _f64(K), _f64(V)
     shape = Q.shape
     N, d = shape[-2], shape[-1]
@@ -120,7 +123,7 @@ def forward(Q, K, V, m, iters=6, mode=0, scale=None, n_threads=0, diag=False):
     if scale is None:
         scale = default_scale(d)
     O = np.zeros(shape, dtype=np.float64)
-    dg = np.zeros((units, 2), dtype=np.float64) if diag else None
+    dg = np.zeros((units, 3), dtype=np.float64) if diag else None
     rc = _load().oracle_forward(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), units, N, d, m, iters,
                                 mode, float(scale), int(n_threads), _ptr(dg))
     _check(rc, "forward")

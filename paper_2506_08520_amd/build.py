@@ -1,5 +1,17 @@
 """Build step of the HIP library: compiles csrc/*.hip for gfx950 into
-libnystra.so inside the package (in-tree, so it travels with the sources)."""
+libnystra.so inside the package (in-tree, so it travels with the sources).
+
+With NYSTRA_SANITIZE_HOST=1 in the environment the HOST code (the C-ABI layer:
+validation, dispatch, launch) is built with AddressSanitizer and
+UndefinedBehaviorSanitizer; device code is unchanged.  Such a library is for
+the host-only tests, loaded with clang's ASan runtime preloaded:
+
+    NYSTRA_SANITIZE_HOST=1 python paper_2506_08520_amd/build.py
+    LD_PRELOAD=$(ls /opt/rocm/llvm/lib/clang/*/lib/linux/libclang_rt.asan-x86_64.so) \
+        ASAN_OPTIONS=detect_leaks=0 python -m pytest tests/test_abi_host.py
+
+Rebuild without the variable afterwards.
+"""
 import concurrent.futures as cf
 import os
 import subprocess
@@ -23,9 +35,19 @@ FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-Wall", "-Werr
          "-I", os.path.join(os.path.dirname(HERE), "include")]
 
 
+# Host-side sanitizers (each option marked for the host compilation only).
+HOST_SANITIZE = ["-Xarch_host", "-fsanitize=address,undefined",
+                 "-Xarch_host", "-fno-sanitize-recover=undefined",
+                 "-Xarch_host", "-fno-omit-frame-pointer"]
+
+
+def _sanitize():
+    return HOST_SANITIZE if os.environ.get("NYSTRA_SANITIZE_HOST") == "1" else []
+
+
 def _compile(src, verbose):
     obj = os.path.join(OBJDIR, src.replace(".hip", ".o"))
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *FLAGS, *_sanitize(), "-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -39,7 +61,8 @@ def build(verbose=False, jobs=8):
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
         objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
     tmp = LIB + ".tmp"
-    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *_sanitize()[:2], *objs,
+           "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

@@ -50,6 +50,9 @@ constexpr int kMaxN = 1 << 20;
 constexpr int kMaxD = 64;
 constexpr int kMaxM = 64;
 constexpr int kMaxIters = 64;
+// Units per call: every kernel's grid is at most 256 work-items per unit in its
+// x dimension, and a launch holds fewer than 2^32 work-items per dimension.
+constexpr int64_t kMaxUnits = (int64_t(1) << 24) - 1;
 
 thread_local char g_last_error[256] = "";
 
@@ -77,7 +80,7 @@ int check_common(int n_windows, int heads, int N, int d, int dtype, int64_t *uni
     if (n_windows < 0 || heads < 0 || N < 1 || N > kMaxN || d < 1 || d > kMaxD)
         return NYSTRA_ERR_SHAPE;
     const int64_t u = int64_t(n_windows) * int64_t(heads);
-    if (u > int64_t(INT32_MAX))
+    if (u > kMaxUnits)
         return NYSTRA_ERR_SHAPE;
     *units = u;
     return NYSTRA_OK;
@@ -97,6 +100,11 @@ int check_tensors(const void *Q, const void *K, const void *V, const void *O, in
         return NYSTRA_ERR_OVERLAP;
     return NYSTRA_OK;
 }
+
+// hipGetLastError() reports the last error of any HIP call on this thread.
+// Each entry point clears it right before its first launch, so that the
+// status it returns speaks of its own launches only.
+void clear_stale_error() { (void)hipGetLastError(); }
 
 int finish_launch(hipError_t e)
 {
@@ -204,6 +212,7 @@ int nystra_attn_forward_ex(const void *Q, const void *K, const void *V, void *O,
     if (rc != NYSTRA_OK)
         return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    clear_stale_error();
     if (variant == NYSTRA_VARIANT_TILED)
         return finish_launch(nystra::launch_tiled_forward(p, s));
     return finish_launch(nystra::launch_generic_forward(p, s));
@@ -251,8 +260,10 @@ int nystra_attn_forward_ws(const void *Q, const void *K, const void *V, void *O,
         if (overlaps(workspace, wn, Q, bytes) || overlaps(workspace, wn, K, bytes) ||
             overlaps(workspace, wn, V, bytes) || overlaps(workspace, wn, O, bytes))
             return NYSTRA_ERR_WORKSPACE;
+        clear_stale_error();
         return finish_launch(nystra::launch_split(p, workspace, s));
     }
+    clear_stale_error();
     if (variant == NYSTRA_VARIANT_TILED)
         return finish_launch(nystra::launch_tiled_forward(p, s));
     return finish_launch(nystra::launch_generic_forward(p, s));
@@ -292,6 +303,7 @@ int nystra_exact_attn_forward(const void *Q, const void *K, const void *V, void 
     p.m = 0;
     p.dtype = dtype;
     p.scale = scale > 0.f ? scale : float(1.0 / sqrt(double(d_h)));
+    clear_stale_error();
     return finish_launch(nystra::launch_exact(p, static_cast<hipStream_t>(stream)));
 }
 
@@ -332,6 +344,7 @@ int nystra_landmark_pool(const void *Q, const void *K, float *Qbar, float *Kbar,
     p.m = m;
     p.dtype = dtype;
     p.geo = g;
+    clear_stale_error();
     return finish_launch(
         nystra::launch_landmark_pool(p, Qbar, Kbar, map, static_cast<hipStream_t>(stream)));
 }
@@ -492,6 +505,7 @@ int nystra_block_forward(const void *X, const void *Wqkv, const void *bqkv, cons
     g.out0 = q;
     g.out1 = k;
     g.out2 = v;
+    clear_stale_error();
     hipError_t e = nystra::launch_block_gemm(g, st);
     if (e != hipSuccess)
         return finish_launch(e);

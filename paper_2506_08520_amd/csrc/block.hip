@@ -500,6 +500,8 @@ bool try_rk(const BlockArgs &a, hipStream_t stream)
     if (a.rows * int64_t(a.C) >= (int64_t(1) << 31) ||
         int64_t(a.C) * a.ncols >= (int64_t(1) << 31))
         return false;   // 32-bit element offsets
+    if ((a.rows + kRkRows - 1) / kRkRows * 64 * kRkWaves >= (int64_t(1) << 32))
+        return false;   // fewer than 2^32 work-items in the grid
     const uintptr_t wp = uintptr_t(a.wt);
     if (E::bytes == 4 ? (wp % 16 != 0 || a.ncols % 4 != 0) : (wp % 4 != 0 || a.ncols % 2 != 0))
         return false;

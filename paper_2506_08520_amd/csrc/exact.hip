@@ -276,7 +276,9 @@ bool exact_tiled_ok(const Problem &p)
 {
     if (p.N % 32 != 0 || !tiled_width(p.d))
         return false;
-    if (p.units * int64_t((p.N / 16 + kExactWaves - 1) / kExactWaves) > int64_t(INT32_MAX))
+    // fewer than 2^32 work-items in the grid; otherwise the rows kernel runs
+    if (p.units * int64_t((p.N / 16 + kExactWaves - 1) / kExactWaves) * 64 * kExactWaves >=
+        (int64_t(1) << 32))
         return false;
     if (p.dtype == 1) {
         const uintptr_t mis = uintptr_t(p.q) | uintptr_t(p.k) | uintptr_t(p.v);

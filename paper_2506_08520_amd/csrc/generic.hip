@@ -1,5 +1,5 @@
 // Portable PnP-Nystra kernels: one 256-thread workgroup per (window, head)
-// unit, every shape within the library limits (N <= 4096, d_h <= 64, m <= 64),
+// unit, every shape within the library limits (N <= 2^20, d_h <= 64, m <= 64),
 // fp32 vector arithmetic, LDS for the small per-unit matrices.  They are the
 // fallback behind the MFMA-tiled kernels and the reference the tiled kernels
 // are compared against on shapes both cover.

@@ -88,7 +88,8 @@ def test_forward_validation(L):
     assert fwd(L, dtype=-1) == EDTYPE
     for kw in [dict(N=0), dict(N=(1 << 20) + 1), dict(d=0), dict(d=65), dict(m=0), dict(m=65, N=4096),
                dict(m=65), dict(W=-1), dict(H=-2), dict(N=63, m=7), dict(N=64, m=3),
-               dict(W=1 << 16, H=1 << 16)]:
+               dict(W=1 << 16, H=1 << 16), dict(W=1 << 24, H=1), dict(W=1 << 23, H=2),
+               dict(W=(1 << 23) + 1, H=2)]:
         assert fwd(L, **kw) == ESHAPE, kw
     seg = B.make_opts(landmark_mode=1)
     assert fwd(L, N=64, m=5, opts=seg) == ESHAPE

@@ -1,23 +1,33 @@
 """GPU parity of the window-attention block (nystra_block_forward) against
 the float64 block oracle: projections, window partition with cyclic shift,
 head split and merge, window reverse, around PnP-Nystra or exact attention.
-Bars: fp32 max-abs <= 1e-4; bf16 max-abs <= 2e-2 x RMS after allowing every
-element the half bf16 ulp that storing it costs.  A bf16 block stores three
-times (Q/K/V, the attention output, Y), and the GPU rounds fp32 values where
-the oracle rounds float64 ones, so an element within fp32 noise of a rounding
-boundary may land one bf16 ulp away; on Y's heavy tail one ulp is already
-~2% of RMS."""
+Bars (helpers.check): fp32 max-abs <= 1e-4.  bf16: max-abs <= 2e-2 x RMS
+wherever the oracle's own bf16 rounding of Y meets that bar, and the error
+beyond the rounding of Y <= BLOCK_BEYOND_BF16 = 2e-2 x RMS.  The oracle's Y is
+taken before its own final rounding, so that the bars see the GPU's rounding
+of Y as a rounding.  A bf16 block stores three times (Q/K/V, the attention
+output, Y) as a bf16 model does, and the block oracle rounds Q/K/V and the
+attention output at the same places -- but from float64 values, where the GPU
+rounds fp32 GEMM and attention results.  An element whose value
+lies within that fp32 error of a bf16 rounding midpoint is stored one bf16
+ulp apart on the two sides, and such flips of intermediate tensors carry into
+Y (measured: 0.66-1.4e-2 of RMS beyond the rounding of Y).  The kernels' own
+precision is held to the 2e-3 bar by the operator tests, where the inputs are
+stored exactly."""
 import numpy as np
 import pytest
 
 from oracle import block as OB
 from paper_2506_08520_amd import binding as B
 from paper_2506_08520_amd import workloads as W
-from helpers import TOL, error, to_dev, to_host
+from helpers import TOL, check, error, to_dev, to_host
 
 pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
+
+
+BLOCK_BEYOND_BF16 = 2e-2
 
 
 def run_block(inputs, heads, window, shift, m, dtype, attention, mode=0, iters=6, nobias=False):
@@ -58,11 +68,9 @@ def test_block_parity(case):
     Bn, H, Wd, C, heads, w, s, m, dtype, att = case
     inputs = W.block_inputs(Bn, H, Wd, C, seed=H * Wd + C + s, dtype=dtype)
     ref = OB.block_forward(*inputs, heads=heads, window=w, shift=s, m=max(m, 1), attention=att,
-                           dtype=dtype)
+                           dtype=dtype, round_output=False)
     got = run_block(inputs, heads, w, s, m, dtype, att)
-    err = error(got, ref, dtype, storage_floor=dtype == "bf16")
-    print(f"{case}: error {err:.3e} (literal {error(got, ref, dtype):.3e})")
-    assert err <= TOL[dtype]
+    check(got, ref, dtype, f"block {case}", beyond_bar=BLOCK_BEYOND_BF16)
 
 
 def test_block_without_biases_and_segment_pooling():

@@ -85,6 +85,24 @@ def test_pinv_residual_identity():
                 np.testing.assert_allclose(Ek1, pred, rtol=0, atol=1e-12)
 
 
+@pytest.mark.parametrize("K", [0, 1, 3, 6])
+def test_residual_diagnostic(K):
+    """The diagnostic ||I - G_A^n Z_K||_F of the batched oracle, on c1-shaped
+    units, equals the Frobenius norm of E_K from the residual recurrence
+    E_{k+1} = 3/4 E_k^3 + 1/4 E_k^4 started at E_0 = I - A A^T / (||A||_1
+    ||A||_inf): numpy on the unit's core block, no call of the update."""
+    q, k, v = rng(21).standard_normal((3, 3, 64, 30))
+    _, dg = oracle.forward(q, k, v, 16, iters=K, diag=True)
+    assert dg.shape == (3, 3)
+    for u in range(3):
+        A = oracle.unit_trace(q[u], k[u], v[u], 16, iters=0)["GA"]
+        E = np.eye(16) - A @ A.T / (np.abs(A).sum(axis=0).max() * np.abs(A).sum(axis=1).max())
+        for _ in range(K):
+            E = 0.75 * np.linalg.matrix_power(E, 3) + 0.25 * np.linalg.matrix_power(E, 4)
+        np.testing.assert_allclose(dg[u, 2], np.linalg.norm(E, "fro"), rtol=1e-9, atol=1e-12)
+        assert 0 < dg[u, 0] <= dg[u, 1]
+
+
 def test_pinv_start_is_scaled_transpose():
     """Z_0 makes A Z_0 symmetric positive semi-definite with spectrum in (0, 1].
 
