@@ -163,6 +163,27 @@ int nystra_attn_forward_ws(const void *Q, const void *K, const void *V, void *O,
                            const nystra_opts *opts, void *workspace, size_t workspace_bytes,
                            void *stream);
 
+/* For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc: the same
+ * computation and kernel choice as nystra_attn_forward_ws (AUTO may pick the
+ * token-split kernels), with the token-split workspace taken from a static
+ * device array of NYSTRA_STATIC_SCRATCH_BYTES (32 MiB) that the library holds
+ * on every device it runs on, until the process ends (enough for global
+ * attention over a 1024 x 1024 map with 6 heads of 30).  Nothing is
+ * allocated.  The array belongs to the current device; `stream` (NULL = the
+ * null stream) must belong to that device too (NYSTRA_ERR_ARG otherwise).
+ * A call whose token-split workspace would exceed the array returns
+ * NYSTRA_ERR_WORKSPACE before anything is enqueued.  Every call on a device
+ * shares its array, whose contents on entry do not matter and on return are
+ * unspecified: calls that overlap on one device (other streams or threads)
+ * race on it and must be serialised by the caller.  The first call on a
+ * device looks the array's address up (hipGetSymbolAddress). */
+#define NYSTRA_STATIC_SCRATCH_BYTES (32u << 20)
+
+int nystra_attn_forward_noalloc(const void *Q, const void *K, const void *V, void *O,
+                                int n_windows, int heads, int N, int d_h, int m, int dtype,
+                                const nystra_opts *opts, void *stream);
+
 /* Window-attention block around the operator: the structure of Sec. 1 for
  * SwinIR / Uformer-style models, from a feature map X to a feature map Y.
  *   1. the B x H x W map is rolled by -shift in both directions and cut into

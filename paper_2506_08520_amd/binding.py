@@ -22,9 +22,10 @@ EXPORTS = (
     "nystra_default_opts", "nystra_attn_forward", "nystra_attn_forward_ex",
     "nystra_exact_attn_forward", "nystra_landmark_pool", "nystra_landmark_map",
     "nystra_select_variant", "nystra_attn_workspace_size", "nystra_attn_forward_ws",
-    "nystra_block_workspace_size", "nystra_block_forward",
+    "nystra_block_workspace_size", "nystra_block_forward", "nystra_attn_forward_noalloc",
     "nystra_status_str", "nystra_last_error",
 )
+STATIC_SCRATCH_BYTES = 32 << 20   # NYSTRA_STATIC_SCRATCH_BYTES
 BLOCK_NYSTROM, BLOCK_EXACT = 0, 1
 
 
@@ -84,7 +85,9 @@ def lib():
     L.nystra_block_forward.argtypes = ([_vp] * 6 + [ctypes.POINTER(BlockShape), _i, _i,
                                                      ctypes.POINTER(Opts), _i, _vp,
                                                      ctypes.c_size_t, _vp])
-    for name in EXPORTS[:11]:
+    L.nystra_attn_forward_noalloc.argtypes = ([_vp] * 4 + [_i] * 6 +
+                                              [ctypes.POINTER(Opts), _vp])
+    for name in EXPORTS[:12]:
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -181,6 +184,19 @@ def nystra_attn_forward_ws(q, k, v, m, opts=None, workspace=None, out=None, stre
     rc = lib().nystra_attn_forward_ws(_ptr(q), _ptr(k), _ptr(v), _ptr(o), W, H, N, d, m, code,
                                       po, _ptr(workspace), nbytes, _stream(stream))
     _check(rc, "nystra_attn_forward_ws")
+    return o
+
+
+def nystra_attn_forward_noalloc(q, k, v, m, opts=None, out=None, stream=None):
+    """PnP-Nystra through the allocation-free entry point (the token-split
+    workspace is the library's static device array)."""
+    import torch
+    W, H, N, d = _shape(q, k, v)
+    o = torch.empty_like(q) if out is None else out
+    po = ctypes.byref(opts) if opts is not None else None
+    rc = lib().nystra_attn_forward_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(o), W, H, N, d, m,
+                                           _dtype_code(q), po, _stream(stream))
+    _check(rc, "nystra_attn_forward_noalloc")
     return o
 
 

@@ -5,6 +5,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "../../include/nystra.h"
 #include "internal.hpp"
 
@@ -267,6 +269,93 @@ int nystra_attn_forward_ws(const void *Q, const void *K, const void *V, void *O,
     if (variant == NYSTRA_VARIANT_TILED)
         return finish_launch(nystra::launch_tiled_forward(p, s));
     return finish_launch(nystra::launch_generic_forward(p, s));
+}
+
+}  // extern "C"
+
+namespace {
+
+// Scratch of the allocation-free entry point: the token-split workspace as a
+// static device array.  Every device the library runs on holds its own copy
+// at its own address, until the process ends.  In host code `scratch` names a
+// host-side stand-in only; kernels receive the device address looked up below.
+static __device__ __align__(256) unsigned char scratch[NYSTRA_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on device `dev`, looked up once per device with
+// that device current (the caller's current device, checked by the caller).
+hipError_t scratch_address(int dev, void **ptr)
+{
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess)
+            return e;
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" {
+
+int nystra_attn_forward_noalloc(const void *Q, const void *K, const void *V, void *O,
+                                int n_windows, int heads, int N, int d_h, int m, int dtype,
+                                const nystra_opts *opts, void *stream)
+{
+    Problem p;
+    int variant = 0;
+    int rc = build_problem(Q, K, V, O, n_windows, heads, N, d_h, m, dtype, opts, true, &p,
+                           &variant);
+    if (rc != NYSTRA_OK)
+        return rc;
+    if (p.units == 0)
+        return NYSTRA_OK;
+    const int64_t bytes = p.units * N * d_h * dtype_bytes(dtype);
+    rc = check_tensors(Q, K, V, O, bytes, dtype_bytes(dtype));
+    if (rc != NYSTRA_OK)
+        return rc;
+    const size_t need = variant == NYSTRA_VARIANT_SPLIT ? nystra::split_workspace_bytes(p) : 0;
+    if (need > size_t(NYSTRA_STATIC_SCRATCH_BYTES)) {
+        set_last_error("token-split workspace exceeds NYSTRA_STATIC_SCRATCH_BYTES");
+        return NYSTRA_ERR_WORKSPACE;
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    clear_stale_error();
+    if (variant != NYSTRA_VARIANT_SPLIT) {   // these kernels use no scratch memory
+        if (variant == NYSTRA_VARIANT_TILED)
+            return finish_launch(nystra::launch_tiled_forward(p, s));
+        return finish_launch(nystra::launch_generic_forward(p, s));
+    }
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return finish_launch(e);
+    if (dev < 0 || dev >= kMaxDevices) {
+        set_last_error("device index beyond the scratch table");
+        return NYSTRA_ERR_ARG;
+    }
+    if (s) {   // the kernels run on the stream's device; its scratch copy must be the one used
+        int sdev = -1;
+        e = hipStreamGetDevice(s, &sdev);
+        if (e != hipSuccess)
+            return finish_launch(e);
+        if (sdev != dev) {
+            set_last_error("stream does not belong to the current device");
+            return NYSTRA_ERR_ARG;
+        }
+    }
+    void *ws = nullptr;
+    e = scratch_address(dev, &ws);
+    if (e != hipSuccess)
+        return finish_launch(e);
+    return finish_launch(nystra::launch_split(p, ws, s));
 }
 
 int nystra_attn_forward(const void *Q, const void *K, const void *V, void *O, int n_windows,

@@ -243,6 +243,24 @@ def bshape(**kw):
                                          "window", "shift")))
 
 
+def test_noalloc_rejects_more_than_its_scratch(L):
+    """The allocation-free entry point refuses, before any launch, a call
+    whose token-split workspace exceeds its static array."""
+    opts = B.make_opts(variant=B.VARIANT_SPLIT)
+    W_, H_, N_, d_, m_ = 16, 6, 262144, 30, 64
+    assert B.nystra_attn_workspace_size(W_, H_, N_, d_, m_, 0, opts) > B.STATIC_SCRATCH_BYTES
+    assert B.nystra_attn_workspace_size(1, 6, N_, d_, m_, 0, opts) <= B.STATIC_SCRATCH_BYTES
+    step = 1 << 33   # fake, disjoint, aligned device addresses
+    q, k, v, o = (ctypes.c_void_p(step * (i + 1)) for i in range(4))
+    f = L.nystra_attn_forward_noalloc
+    assert f(q, k, v, o, W_, H_, N_, d_, m_, 0, ctypes.byref(opts), None) == EWS
+    assert b"NYSTRA_STATIC_SCRATCH_BYTES" in L.nystra_last_error()
+    # the other validation paths are those of nystra_attn_forward_ws
+    assert f(None, k, v, o, 1, 6, N_, d_, m_, 0, ctypes.byref(opts), None) == ENULL
+    assert f(q, k, v, o, 1, 6, N_, 65, m_, 0, ctypes.byref(opts), None) == ESHAPE
+    assert f(q, k, v, o, 0, 6, N_, d_, m_, 0, None, None) == OK
+
+
 def test_block_workspace_size():
     one = 16 * 16 * 96 * 4                      # one of Q, K, V, O in fp32 (256-byte multiple)
     assert B.nystra_block_workspace_size(bshape(), 16) == 4 * one
