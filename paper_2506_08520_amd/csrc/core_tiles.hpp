@@ -32,11 +32,19 @@ struct LargeLds {
     static constexpr int ya = zb + RS;
     static constexpr int yb = ya + RS;                  // also the own-row transpose scratch
     static constexpr int vec = yb + RS;                 // [MT][64]
+    // Before the landmark core runs, its matrix regions hold the key pass of
+    // the one-pass large kernel: the Qbar table and one record per wave (T
+    // rows of every landmark, pitch kRecP; T_D; running maxima).
+    static constexpr int kRecP = 32;
+    static constexpr int rec_len = M * kRecP + 2 * M;
+    static constexpr int qtab = zb;
+    static constexpr int recs = qtab + M * kTS;
     static constexpr int tab_len = M * kTS + M;         // table + its denominator column
     static constexpr bool tab_in_y = tab_len <= RS;     // T in ya, W in yb after the iteration
     static constexpr int tb = tab_in_y ? ya : vec + MT * 64;
     static constexpr int wb = tab_in_y ? yb : tb + tab_len;
     static constexpr int total = tab_in_y ? vec + MT * 64 : wb + tab_len;
+    static_assert(recs + MT * rec_len <= vec, "key-pass records fit the core's regions");
 };
 
 // Right-hand operand (D-layout) of tile (a, b) of a row-major LDS matrix.

@@ -6,9 +6,11 @@
 //   1. Step 1: each lane averages the patch of its own landmark straight from
 //      global memory (any pooling grid), producing Qbar rows in registers and
 //      Kbar rows in LDS.
-//   2. Step 3, G_U side: the wave streams all N keys once, keeping the row
-//      maxima m_U of its landmarks as running maxima and accumulating
-//      G_U^n and T = G_U^n [V | 1], rescaled whenever a maximum grows.
+//   2. Step 3, G_U side: the waves split the keys, each wave covering every
+//      landmark tile: running maxima of S_U over its keys, and G_U^n and
+//      T = G_U^n [V | 1] accumulated against them (rescaled whenever a maximum
+//      grows).  The waves' records are merged in LDS against the row maxima
+//      m_U over all keys.  Every K and V row is read once per unit.
 //   3. Step 2 and Step 4: the wave builds its row tile of A = G_A^n; the m x m
 //      pseudo-inverse iteration runs with each wave computing its row tile of
 //      every product, the right-hand operands exchanged through LDS.
@@ -51,7 +53,8 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     extern __shared__ float lds[];
     float *kbar = lds + L::kbar;
 
-    const int lt = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    // the wave index is uniform: keep it (and the loops it bounds) scalar
+    const int lt = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
     const int g = lane >> 4, c = lane & 15;
     float *vec = lds + L::vec + 64 * lt;
     const int m = FULL ? 16 * MT : a.m, N = a.N, NT = a.N >> 4;
@@ -122,48 +125,58 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         if (slot_valid<D>(g, s))
             kbar[l * kTS + chunk_start<D>(g) + s] = kbv[s];
 
-    // ---- Step 3, G_U side, one pass over the N keys, kGroup key tiles per
-    // step: m_U of this landmark as a running maximum, and G_U^n and
-    // T = G_U^n [V | 1] accumulated against it; when the maximum grows, the
-    // partial T and T_D are rescaled by exp(old - new), so that at the end they
-    // hold exactly the sums against the final m_U.
-    constexpr int kGroup = 4;
+    // Qbar rows go to a table too, so that every wave can read every tile.
+    float *qtab = lds + L::qtab;
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+        if (slot_valid<D>(g, s))
+            qtab[l * kTS + chunk_start<D>(g) + s] = qb[s];
+    __syncthreads();   // Qbar and Kbar complete
+
+    // ---- Step 3, G_U side.  The waves split the keys: wave lt takes the key
+    // tile pairs 2lt, 2lt + 2MT, ... and, for every landmark tile j, keeps the
+    // running maximum of S_U over its keys and T_j = G_U^n [V | 1] and T_D
+    // accumulated against it (rescaled by exp(old - new) whenever a maximum
+    // grows).  The waves' records are then merged against the largest of
+    // their maxima, m_U: the sums of Step 3 against the row maxima over all N
+    // keys, only added in another order.  Every K and V row is read once.
+    constexpr int NCT = (D + 15) / 16;   // feature tiles of T (the ones column included)
+    constexpr int kRecP = L::kRecP, LD = L::M * kRecP, LM = LD + L::M;
     const uint16_t *ku16 = reinterpret_cast<const uint16_t *>(ku);
-    bf8 qbh, qbl;   // bf16 path: Qbar row as hi + lo terms
-    if constexpr (BFM)
-        split_bf16(qb, qbh, qbl);
-    // S_U^T tile for key tile tt: lane (g,c) gets S_U[landmark l][key 16tt + 4g + i].
-    auto su_tile = [&](int tt, const float *kr, const bf8 &kraw) {
-        f4 acc = {0.f, 0.f, 0.f, 0.f};
-        if constexpr (BFM) {
-            acc = mfma_bf16(kraw, qbh, acc);
-            acc = mfma_bf16(kraw, qbl, acc);
-        } else {
-#pragma unroll
-            for (int s = 0; s < 8; ++s)
-                acc = mfma4(kr[s], qb[s], acc);
-        }
-        return acc;
-    };
-    // T[ct] lane (g,c): T[landmark 16lt+4g+i][feature 16ct+c].
-    f4 T[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-    float tden = 0.f;    // this lane's share of T_D of landmark l
-    float mrun = -INFINITY;   // running max of S_U[l][.] (unscaled logits)
     const uint16_t *vu16 = reinterpret_cast<const uint16_t *>(vu);
-    // Key groups are software-pipelined: the loads of group t0 + kGroup are
-    // issued before group t0 is computed (past the end they repeat the last
-    // tile and go unused).  Chunks are loaded raw, so no instruction waits on
-    // a load at its issue.
-    // bf16 V is held as pairs of rows (4g, 4g+1) and (4g+2, 4g+3) of one
-    // column, the two 16-bit loads landing in the halves of one register.
-    typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
-    float kr[kGroup][8], vr[kGroup][2][4], krn[kGroup][8], vrn[kGroup][2][4];
-    bf8 kw[kGroup], kwn[kGroup];
-    uint32_t vh[kGroup][2][2], vhn[kGroup][2][2];
-    auto load_group = [&](int t0, float (&kr_)[kGroup][8], bf8 (&kw_)[kGroup],
-                          float (&vr_)[kGroup][2][4], uint32_t (&vh_)[kGroup][2][2]) {
+    float qj[MT][8];   // Qbar rows of every landmark tile: lane (g, c) holds landmark 16j + c
+    bf8 qjh[MT], qjl[MT];
 #pragma unroll
-        for (int u = 0; u < kGroup; ++u) {
+    for (int j = 0; j < MT; ++j) {
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+            qj[j][s] = slot_valid<D>(g, s) ? qtab[(16 * j + c) * kTS + chunk_start<D>(g) + s]
+                                           : 0.f;
+        if constexpr (BFM)
+            split_bf16(qj[j], qjh[j], qjl[j]);
+    }
+    f4 TJ[MT][NCT];
+    float tdj[MT], mrj[MT];
+#pragma unroll
+    for (int j = 0; j < MT; ++j) {
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct)
+            TJ[j][ct] = f4{0.f, 0.f, 0.f, 0.f};
+        tdj[j] = 0.f;
+        mrj[j] = -INFINITY;
+    }
+    // Pairs are software-pipelined: the next pair's K and V rows are requested
+    // before this pair is computed (past the end they repeat the last tile,
+    // unused).  bf16 V is held as pairs of rows (4g, 4g+1) and (4g+2, 4g+3) of
+    // one column, the two 16-bit loads landing in the halves of one register.
+    typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+    float kr[2][8], vr[2][NCT][4], krn[2][8], vrn[2][NCT][4];
+    bf8 kw[2], kwn[2];
+    uint32_t vh[2][NCT][2], vhn[2][NCT][2];
+    auto load_pair = [&](int t0, float (&kr_)[2][8], bf8 (&kw_)[2], float (&vr_)[2][NCT][4],
+                         uint32_t (&vh_)[2][NCT][2]) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
             // 32-bit offsets from the unit's (uniform) base: N d < 2^26
             const int tt = min(t0 + u, NT - 1);
             const unsigned row = unsigned(16 * tt + c) * d;
@@ -174,135 +187,221 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             else   // bf16 values through the fp32 path: unpacked (and masked) here
                 load_chunk8<E, D>(ku + row, g, kr_[u]);
 #pragma unroll
-            for (int ct = 0; ct < 2; ++ct) {
+            for (int ct = 0; ct < NCT; ++ct) {
                 const int f = 16 * ct + c;
-                // Columns past d repeat column d - 1: they reach only columns
-                // of T, W and O that are never stored (T_D is summed apart).
                 // one address per row group; the four rows are immediate offsets
                 const unsigned vrow = unsigned(16 * tt + 4 * g) * d + unsigned(min(f, d - 1));
-                const uint16_t *vp16 = vu16 + vrow;
-                const typename E::T *vp = vu + vrow;
                 if constexpr (BFM) {
 #pragma unroll
-                    for (int p = 0; p < 2; ++p) {
+                    for (int pp = 0; pp < 2; ++pp) {
                         u16x2 pr;
-                        pr.x = vp16[2 * p * d];
-                        pr.y = vp16[(2 * p + 1) * d];
-                        vh_[u][ct][p] = __builtin_bit_cast(uint32_t, pr);
+                        pr.x = vu16[vrow + 2 * pp * d];
+                        pr.y = vu16[vrow + (2 * pp + 1) * d];
+                        vh_[u][ct][pp] = __builtin_bit_cast(uint32_t, pr);
                     }
                 } else {
 #pragma unroll
-                    for (int s = 0; s < 4; ++s)
-                        vr_[u][ct][s] = E::load(vp, s * d);
+                    for (int x = 0; x < 4; ++x)
+                        vr_[u][ct][x] = E::load(vu + vrow, x * d);
                 }
             }
         }
     };
-    // One group of key tiles: masks, logits, running maxima, G_U^n and T.
-    // The K chunks stay unmasked: their overlapping slots meet zeros in the
-    // Qbar slots (Step 1 zeroes them).
-    auto process = [&](int t0, float (&kr)[kGroup][8], bf8 (&kw)[kGroup],
-                       float (&vr)[kGroup][2][4], uint32_t (&vh)[kGroup][2][2]) {
-        if constexpr (PAD) {
-            const bool ones = c == D % 16;   // column D, in feature tile D / 16
+    // One pair of key tiles for every landmark tile: ones column, logits,
+    // running maxima, G_U^n and T.  The K chunks stay unmasked: their
+    // overlapping slots meet zeros in the Qbar slots.
+    auto process = [&](int t0, float (&kr_)[2][8], bf8 (&kw_)[2], float (&vr_)[2][NCT][4],
+                       uint32_t (&vh_)[2][NCT][2]) {
 #pragma unroll
-            for (int u = 0; u < kGroup; ++u) {
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) {
+                const int f = 16 * ct + c;
                 if constexpr (BFM) {
 #pragma unroll
-                    for (int p = 0; p < 2; ++p)
-                        vh[u][D / 16][p] = ones ? 0x3F803F80u : vh[u][D / 16][p];   // bf16 1.0, twice
+                    for (int pp = 0; pp < 2; ++pp)
+                        vh_[u][ct][pp] = f < d ? vh_[u][ct][pp]
+                                               : (PAD && f == d ? 0x3F803F80u : 0u);
                 } else {
 #pragma unroll
                     for (int x = 0; x < 4; ++x)
-                        vr[u][D / 16][x] = ones ? 1.f : vr[u][D / 16][x];
+                        vr_[u][ct][x] = f < d ? vr_[u][ct][x] : (PAD && f == d ? 1.f : 0.f);
                 }
             }
-        }
-        // Logits of the group (a repeated last tile leaves the maximum unchanged
-        // and is not accumulated).
-        f4 su[kGroup];
-        float gmax = -INFINITY;
-#pragma unroll
-        for (int u = 0; u < kGroup; ++u) {
-            su[u] = su_tile(min(t0 + u, NT - 1), kr[u], kw[u]);
-            gmax = fmaxf(gmax, fmaxf(fmaxf(su[u][0], su[u][1]), fmaxf(su[u][2], su[u][3])));
-        }
-        const float mnew = fmaxf(mrun, max_groups(gmax));
-        {   // rescale what is accumulated: factor 1 exactly when the maximum
-            // holds, 0 on the first group (all lanes take part in the exchange)
-            const float f = fast_exp2(a.s2 * (mrun - mnew));
-            tden *= f;
-            const f4 fr = by_rows(f, vec, g, c);   // factor of landmark 16lt+4g+i
-            T[0] *= fr;
-            T[1] *= fr;
-        }
-        mrun = mnew;
-        const float mb = a.s2 * mnew;
+        const bool second = t0 + 1 < NT;   // uniform
+        bf8 vv[NCT];   // bf16 path: V of the pair as the right-hand operand
         if constexpr (BFM) {
-            // Key tiles in pairs: the bf16 product contracts 32 keys, lane group g
-            // supplying keys 4g..4g+3 of both tiles.  N % 32 == 0 on this path.
 #pragma unroll
-            for (int u = 0; u < kGroup; u += 2) {
-                if (t0 + u >= NT)
-                    break;   // uniform
+            for (int ct = 0; ct < NCT; ++ct) {
+                U16B vb;
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj)
+                    vb.w[jj] = vh_[jj >> 1][ct][jj & 1];
+                vv[ct] = __builtin_bit_cast(bf8, vb);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < MT; ++j) {
+            // S_U^T tiles: lane (g, c) gets S_U[landmark 16j + c][key 16tt + 4g + i].
+            f4 su[2];
+            float gmax = -INFINITY;
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                f4 acc = {0.f, 0.f, 0.f, 0.f};
+                if constexpr (BFM) {
+                    acc = mfma_bf16(kw_[u], qjh[j], acc);
+                    acc = mfma_bf16(kw_[u], qjl[j], acc);
+                } else {
+#pragma unroll
+                    for (int x = 0; x < 8; ++x)
+                        acc = mfma4(kr_[u][x], qj[j][x], acc);
+                }
+                su[u] = acc;
+                // a repeated last tile (fp32 path, odd tile count) leaves the
+                // maximum unchanged, so it needs no exclusion here
+                gmax = fmaxf(gmax, fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3])));
+            }
+            const float mnew = fmaxf(mrj[j], max_groups(gmax));
+            // Rescale what is accumulated when a maximum grew; the factor is
+            // exactly 1 for every landmark whose maximum held, so skipping the
+            // step when none grew changes nothing.
+            if (__builtin_amdgcn_ballot_w64(mnew != mrj[j]) != 0) {
+                const float f = fast_exp2(a.s2 * (mrj[j] - mnew));
+                tdj[j] *= f;
+                const f4 fr = by_rows(f, vec, g, c);   // factor of landmark 16j + 4g + i
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct)
+                    TJ[j][ct] *= fr;
+            }
+            mrj[j] = mnew;
+            // Landmarks past m get an infinite offset: their terms are exactly 0.
+            const float mb = (FULL || 16 * j + c < m) ? a.s2 * mnew : INFINITY;
+            if constexpr (BFM) {
+                // bf16 product over the 32 keys of the pair, lane group g
+                // supplying keys 4g..4g+3 of both tiles (N % 32 == 0 here)
                 float gk[8];
 #pragma unroll
                 for (int h = 0; h < 2; ++h)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        gk[4 * h + i] = lval ? fast_exp2(fmaf(a.s2, su[u + h][i], -mb)) : 0.f;
+                        gk[4 * h + i] = fast_exp2(fmaf(a.s2, su[h][i], -mb));
                         if constexpr (!PAD)
-                            tden += gk[4 * h + i];
+                            tdj[j] += gk[4 * h + i];
                     }
                 bf8 gh, gl;
                 split_bf16(gk, gh, gl);
 #pragma unroll
-                for (int ct = 0; ct < 2; ++ct) {
-                    U16B vb;
-#pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        vb.w[j] = vh[u + (j >> 1)][ct][j & 1];
-                    const bf8 vv = __builtin_bit_cast(bf8, vb);
-                    T[ct] = mfma_bf16(gh, vv, T[ct]);
-                    T[ct] = mfma_bf16(gl, vv, T[ct]);
+                for (int ct = 0; ct < NCT; ++ct) {
+                    TJ[j][ct] = mfma_bf16(gh, vv[ct], TJ[j][ct]);
+                    TJ[j][ct] = mfma_bf16(gl, vv[ct], TJ[j][ct]);
                 }
-            }
-        } else {
+            } else {
 #pragma unroll
-            for (int u = 0; u < kGroup; ++u) {
-                if (t0 + u >= NT)
-                    break;   // uniform
-                f4 e;
+                for (int u = 0; u < 2; ++u) {
+                    if (u == 1 && !second)
+                        break;   // uniform
+                    f4 e;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    e[i] = lval ? fast_exp2(fmaf(a.s2, su[u][i], -mb)) : 0.f;
-                    if constexpr (!PAD)
-                        tden += e[i];
+                    for (int i = 0; i < 4; ++i) {
+                        e[i] = fast_exp2(fmaf(a.s2, su[u][i], -mb));
+                        if constexpr (!PAD)
+                            tdj[j] += e[i];
+                    }
+#pragma unroll
+                    for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                        for (int x = 0; x < 4; ++x)
+                            TJ[j][ct] = mfma4(e[x], vr_[u][ct][x], TJ[j][ct]);
                 }
-#pragma unroll
-                for (int ct = 0; ct < 2; ++ct)
-#pragma unroll
-                    for (int s = 0; s < 4; ++s)
-                        T[ct] = mfma4(e[s], vr[u][ct][s], T[ct]);
             }
         }
     };
-    // Unrolled by two with two buffers, so that no loaded row is copied.
-    load_group(0, kr, kw, vr, vh);
-    for (int t0 = 0; t0 < NT; t0 += 2 * kGroup) {
-        load_group(t0 + kGroup, krn, kwn, vrn, vhn);
-        process(t0, kr, kw, vr, vh);
-        if (t0 + kGroup >= NT)
-            break;   // uniform
-        load_group(t0 + 2 * kGroup, kr, kw, vr, vh);
-        process(t0 + kGroup, krn, kwn, vrn, vhn);
+    // Unrolled by two with two buffers (no loaded row is copied) where the
+    // registers allow it; bf16 with three or four landmark tiles copies the
+    // prefetched pair instead.
+    load_pair(2 * lt, kr, kw, vr, vh);
+    if constexpr (!(BFM && MT >= 3)) {
+        for (int t0 = 2 * lt; t0 < NT; t0 += 4 * MT) {
+            load_pair(t0 + 2 * MT, krn, kwn, vrn, vhn);
+            process(t0, kr, kw, vr, vh);
+            if (t0 + 2 * MT >= NT)
+                break;   // uniform
+            load_pair(t0 + 4 * MT, kr, kw, vr, vh);
+            process(t0 + 2 * MT, krn, kwn, vrn, vhn);
+        }
+    } else {
+        for (int t0 = 2 * lt; t0 < NT; t0 += 2 * MT) {
+            load_pair(t0 + 2 * MT, krn, kwn, vrn, vhn);
+            process(t0, kr, kw, vr, vh);
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                kw[u] = kwn[u];
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                    for (int x = 0; x < 2; ++x)
+                        vh[u][ct][x] = vhn[u][ct][x];
+            }
+        }
+    }
+    // This wave's record: T rows of every landmark, T_D and the maxima.  An
+    // idle wave (fewer key pairs than waves) leaves -inf maxima, which the
+    // merge weighs by exp2(-inf) = 0.
+    {
+        float *rw = lds + L::recs + lt * L::rec_len;
+#pragma unroll
+        for (int j = 0; j < MT; ++j) {
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    rw[(16 * j + 4 * g + i) * kRecP + 16 * ct + c] = TJ[j][ct][i];
+            const float td = PAD ? 0.f : sum_groups(tdj[j]);
+            if (g == 0) {
+                rw[LD + 16 * j + c] = td;
+                rw[LM + 16 * j + c] = mrj[j];
+            }
+        }
+    }
+    __syncthreads();
+    // Merge for this wave's landmark tile lt: m_U = the largest of the
+    // waves' maxima; T and T_D = sum over waves of exp(s (max_w - m_U)) x
+    // the wave's sums.
+    f4 T[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+    float tden = 0.f, mrun = -INFINITY;
+    f4 mrows = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};   // m_U of landmarks 16lt+4g+i
+    {
+        const float *rb = lds + L::recs;
+#pragma unroll
+        for (int w = 0; w < MT; ++w) {
+            const float *rw = rb + w * L::rec_len;
+            mrun = fmaxf(mrun, rw[LM + l]);
+            const f4 mw = *reinterpret_cast<const f4 *>(rw + LM + 16 * lt + 4 * g);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                mrows[i] = fmaxf(mrows[i], mw[i]);
+        }
+#pragma unroll
+        for (int w = 0; w < MT; ++w) {
+            const float *rw = rb + w * L::rec_len;
+            const float fl = fast_exp2(a.s2 * (rw[LM + l] - mrun));   // 0 for an idle wave
+            tden = fmaf(fl, PAD ? rw[(16 * lt + c) * kRecP + D] : rw[LD + l], tden);
+            const f4 mw = *reinterpret_cast<const f4 *>(rw + LM + 16 * lt + 4 * g);
+            f4 fr;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                fr[i] = fast_exp2(a.s2 * (mw[i] - mrows[i]));
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) {
+                f4 x;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    x[i] = rw[(16 * lt + 4 * g + i) * kRecP + 16 * ct + c];
+                T[ct] += fr * x;
+            }
+        }
     }
     const float mu = a.s2 * mrun;   // m_U of landmark l (base-2 units)
-    // T_D of landmark l (with the ones column it is column D of T, and the
-    // core's separate W_D goes unused)
-    if constexpr (!PAD)
-        tden = sum_groups(tden);
-    __syncthreads();           // Kbar complete
 
     landmark_core<MT, D, BFM, FULL>(lds, qb, mu, T, tden, m, a.iters, a.s2, lt, lane);
     constexpr int TDo = table_den<MT>();
