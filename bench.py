@@ -53,6 +53,10 @@ def parse():
                     help="config:dtype pairs timed besides the headline, one record each")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the same-traffic elementwise kernel (the practical HBM ceiling)")
+    ap.add_argument("--graph", action="store_true",
+                    help="time one replay of a HIP graph holding the timed launches instead "
+                         "of launches issued one by one (measured slower on the 64-token "
+                         "layer: c2 fp32 46.5 us against 43.6)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="wall-clock budget of each CPU-baseline leg (all threads, one thread)")
     ap.add_argument("--sweep", action="store_true",
@@ -90,47 +94,65 @@ class Case:
             self.sets.append((*trip, torch.empty_like(base[0])))
 
 
-def time_kernel(case, launch, steps, warmup, preheat=0.0):
+def time_kernel(case, launch, steps, warmup, preheat=0.0, graph=False):
     """Preheat for `preheat` seconds and run `warmup` untimed launches, then
-    time exactly `steps` back-to-back launches.
+    time exactly `steps` launches, one per step, back to back.
+
+    The launches are issued one by one on a side stream; with graph they are
+    captured once in a HIP graph (stream capture over the rotating buffers)
+    and the timed region is one replay of it.
 
     Returns (ms per step by the host clock between the synchronisations that
-    bracket the timed launches, ms per launch from one HIP event pair around
-    the same launches, and -- as a diagnostic only -- the 10th, 50th and 90th
-    percentiles of event pairs recorded around each launch of a second pass,
-    which also count the events' own overhead).  All events are recorded on
-    the stream the kernels are launched on."""
+    bracket the timed region, ms per launch from one HIP event pair recorded
+    on the launch stream around the same region, and -- as a diagnostic only
+    -- the 10th, 50th and 90th percentiles of event pairs recorded around
+    single eager launches, which include the events' and the host's own
+    overhead, and the number of preheat launches)."""
     import torch
-    stream = torch.cuda.current_stream()
-    # The first launches after idle run at lower clocks (c2 fp32: 51.7 us
-    # after 20 launches, 46.3 us after a second of them); the preheat runs
-    # the same launches for the given time, checked every 64 launches.
-    heat, t_end = 0, time.perf_counter() + preheat
-    while time.perf_counter() < t_end:
-        for _ in range(64):
-            launch(*case.sets[heat % case.nsets], stream)
-            heat += 1
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(stream):
+        # The first launches after idle run at lower clocks (c2 fp32: 51.7 us
+        # after 20 launches, 46.3 us after a second of them); the preheat runs
+        # the same launches for the given time, checked every 64 launches.
+        heat, t_end = 0, time.perf_counter() + preheat
+        while time.perf_counter() < t_end:
+            for _ in range(64):
+                launch(*case.sets[heat % case.nsets], stream)
+                heat += 1
+            stream.synchronize()
+        for i in range(warmup):
+            launch(*case.sets[i % case.nsets], stream)
+        g = None
+        if graph:
+            stream.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=stream):
+                for i in range(steps):
+                    launch(*case.sets[(warmup + i) % case.nsets], stream)
+            g.replay()   # untimed: the first replay uploads the graph
+        r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
-    for i in range(warmup):
-        launch(*case.sets[i % case.nsets], stream)
-    r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    r0.record(stream)
-    for i in range(steps):
-        launch(*case.sets[(warmup + i) % case.nsets], stream)
-    r1.record(stream)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    region = r0.elapsed_time(r1) / steps
-    n = min(steps, 50)
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
-    stops = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
-    for i in range(n):
-        starts[i].record(stream)
-        launch(*case.sets[(warmup + steps + i) % case.nsets], stream)
-        stops[i].record(stream)
-    torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        r0.record(stream)
+        if graph:
+            g.replay()
+        else:
+            for i in range(steps):
+                launch(*case.sets[(warmup + i) % case.nsets], stream)
+        r1.record(stream)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        region = r0.elapsed_time(r1) / steps
+        n = min(steps, 50)
+        starts = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        stops = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        for i in range(n):
+            starts[i].record(stream)
+            launch(*case.sets[(warmup + steps + i) % case.nsets], stream)
+            stops[i].record(stream)
+        torch.cuda.synchronize()
+    del g
     each = sorted(a.elapsed_time(b) for a, b in zip(starts, stops))
     pct = [each[min(n - 1, int(round(f * (n - 1))))] for f in (0.1, 0.5, 0.9)]
     return (t1 - t0) * 1e3 / steps, region, pct, heat
@@ -430,7 +452,8 @@ def measure(wl, dtype, args, q, k, v, headline):
         B.nystra_exact_attn_forward(q_, k_, v_, out=o_, stream=s)
 
     steps = args.steps
-    ms, kern, pairs, heat = time_kernel(case, nys, steps, args.warmup, args.preheat)
+    ms, kern, pairs, heat = time_kernel(case, nys, steps, args.warmup, args.preheat,
+                                        args.graph)
     code = B.F32 if dtype == "f32" else B.BF16
     K = 6
     fl = nystrom_flops(wl.N, wl.d, wl.m, K)
@@ -444,7 +467,8 @@ def measure(wl, dtype, args, q, k, v, headline):
         "variant": {B.VARIANT_GENERIC: "generic", B.VARIANT_TILED: "mfma-tiled"}.get(
             B.nystra_select_variant(wl.N, wl.d, wl.m, code), "?"),
         "kernel_ms": kern, "ms_per_step": ms,
-        "kernel_ms_p10_p50_p90": [float(x) for x in pairs],
+        "timing": "one HIP graph replay of the timed launches" if args.graph else "launches issued one by one",
+        "eager_launch_ms_p10_p50_p90": [float(x) for x in pairs],
         "tokens_per_s": wl.n_windows * wl.N / (kern * 1e-3),
         "unit_tokens_per_s": wl.units * wl.N / (kern * 1e-3),
         "hbm": {"algorithmic_bytes": case.io_bytes, "achieved_GBs": gbs,
@@ -458,11 +482,11 @@ def measure(wl, dtype, args, q, k, v, headline):
     }
     if not args.no_exact:
         ems, ekern, epairs, _ = time_kernel(case, ex, max(10, steps // 4), args.warmup,
-                                            min(args.preheat, 0.3))
+                                            min(args.preheat, 0.3), args.graph)
         ef = floors(wl, dtype, exact_flops(wl.N, wl.d), wl.N * wl.N)
         eb = max(ef, key=ef.get)
         r["exact"] = {"kernel_ms": ekern, "ms_per_step": ems,
-                      "kernel_ms_p10_p50_p90": [float(x) for x in epairs],
+                      "eager_launch_ms_p10_p50_p90": [float(x) for x in epairs],
                       "floor_ms": ef[eb], "floor_bound": eb, "floors_ms": ef,
                       "frac_of_floor": ef[eb] / ekern}
         r["speedup_vs_exact"] = ekern / kern
@@ -475,7 +499,7 @@ def measure(wl, dtype, args, q, k, v, headline):
             torch.addcmul(q_, k_, v_, out=o_)
 
         _, ckern, _, _ = time_kernel(case, same_traffic, steps, args.warmup,
-                                     min(args.preheat, 0.3))
+                                     min(args.preheat, 0.3), args.graph)
         cg = case.io_bytes / (ckern * 1e-3) / 1e9
         r["same_traffic_ceiling"] = {
             "kernel": "torch.addcmul: reads Q, K, V and writes O once, the bytes of one step",

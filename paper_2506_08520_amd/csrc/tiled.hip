@@ -126,27 +126,29 @@ __device__ inline void pool_to_lds(Get get, float *bar, const SmallArgs &a, int 
     }
 }
 
-// Step 1 for a fixed grid, one input: every lane stages its raw chunks (one
-// per token tile) in LDS rows by token, then lane (g, c) adds the chunks of
-// the tokens of landmark c's patch, in patch order: out[s] = patch sum of
-// slot s of group g (zero in overlapping slots and for padding landmarks).
-template <class E, int NT, int D, int GRID, class Chunk>
-__device__ inline void pool_direct(const Chunk (&x)[NT], float *stage, float (&out)[8], int m,
-                                   int g, int c)
+// Stages the raw chunk of token tile tt (this lane's token 16tt + c, feature
+// group g) in the LDS row of its token.
+template <class E, class Chunk>
+__device__ inline void stage_chunk(const Chunk &x, float *stage, int tt, int g, int c)
+{
+    constexpr int RS = raw_stride<E>();
+    float *row = stage + (16 * tt + c) * RS + (E::bytes == 4 ? 8 : 4) * g;
+    if constexpr (E::bytes == 4) {
+        reinterpret_cast<f4 *>(row)[0] = f4{x[0], x[1], x[2], x[3]};
+        reinterpret_cast<f4 *>(row)[1] = f4{x[4], x[5], x[6], x[7]};
+    } else {
+        *reinterpret_cast<U16B *>(row) = __builtin_bit_cast(U16B, x);
+    }
+}
+
+// Lane (g, c) adds the staged chunks of the tokens of landmark c's patch, in
+// patch order: out[s] = patch sum of slot s of group g (zero in overlapping
+// slots and for padding landmarks).
+template <class E, int D, int GRID>
+__device__ inline void patch_sums(const float *stage, float (&out)[8], int m, int g, int c)
 {
     constexpr int RS = raw_stride<E>();
     constexpr int PR = 2, PC = GRID == kGrid2x2 ? 2 : 4, GC = 8 / PC;   // 8 x 8 window
-#pragma unroll
-    for (int tt = 0; tt < NT; ++tt) {
-        float *row = stage + (16 * tt + c) * RS + (E::bytes == 4 ? 8 : 4) * g;
-        if constexpr (E::bytes == 4) {
-            reinterpret_cast<f4 *>(row)[0] = f4{x[tt][0], x[tt][1], x[tt][2], x[tt][3]};
-            reinterpret_cast<f4 *>(row)[1] = f4{x[tt][4], x[tt][5], x[tt][6], x[tt][7]};
-        } else {
-            *reinterpret_cast<U16B *>(row) = __builtin_bit_cast(U16B, x[tt]);
-        }
-    }
-    wave_sync();
     const int le = min(c, m - 1);   // padding lanes read a valid patch, then drop it
     const int r0 = (le / GC) * PR, c0 = (le % GC) * PC;
 #pragma unroll
@@ -174,11 +176,24 @@ __device__ inline void pool_direct(const Chunk (&x)[NT], float *stage, float (&o
                 }
             }
         }
-    wave_sync();
     const bool valid = c < m;
 #pragma unroll
     for (int s = 0; s < 8; ++s)
         out[s] = (valid && slot_keep<D>(g, s)) ? out[s] : 0.f;
+}
+
+// Step 1 for a fixed grid, one input, all NT token tiles held by one wave:
+// stage every chunk, then form the patch sums.
+template <class E, int NT, int D, int GRID, class Chunk>
+__device__ inline void pool_direct(const Chunk (&x)[NT], float *stage, float (&out)[8], int m,
+                                   int g, int c)
+{
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt)
+        stage_chunk<E>(x[tt], stage, tt, g, c);
+    wave_sync();
+    patch_sums<E, D, GRID>(stage, out, m, g, c);
+    wave_sync();
 }
 
 __device__ inline uint32_t pack_bf16x2(float lo, float hi)
@@ -589,6 +604,351 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     }
 }
 
+// ---- 64-token windows, few units: one unit per four-wave workgroup --------
+//
+// When the units are fewer than the SIMDs, one wave per unit leaves most of
+// the chip idle and the launch lasts one unit's whole dependent chain.  Here
+// the four waves of a workgroup split the unit's four token tiles: wave w
+// loads tile w of Q, K and V, and the passes over tokens are shared through
+// LDS -- the staged rows for Step 1, the per-wave maxima of S_U and the
+// per-wave partial sums T_w = G_U^n [V | 1] over the wave's keys (Step 3, G_U
+// side; only the order of the additions changes).  Wave 0 then runs Step 2,
+// the pseudo-inverse and W = Z T (the other waves wait), and every wave forms
+// Steps 3 (G_L side), 6 and 7 for its own tile.  Fixed 8 x 8 pooling grids
+// only (their patches never straddle a token tile).
+
+template <class E, int D>
+struct MwLds {
+    static constexpr int NCT = (D + 15) / 16;
+    static constexpr int RS = raw_stride<E>();
+    static constexpr int qst = 0;                          // [64][RS] raw Q chunks
+    static constexpr int kst = qst + 64 * RS;              // [64][RS] raw K chunks
+    static constexpr int xm = kst + 64 * RS;               // [4][16] maxima of S_U per wave
+    static constexpr int xd = xm + 64;                     // [4][16] T_D per wave
+    static constexpr int xt = xd + 64;                     // [4][NCT][64 lanes][4] T per wave
+    static constexpr int wt = xt + 4 * NCT * 256;          // [NCT][64][4] W, then [64][4] W_D
+    static constexpr int scr = wt + NCT * 256 + 256;       // wave 0's transpose scratch
+    static constexpr int vec = scr + 16 * kTrStride;       // [4][64] row vectors
+    static constexpr int total = vec + 4 * 64;
+};
+
+template <class E, int D, bool BFM, int GRID, int KF>
+__global__ void __launch_bounds__(256)
+tiled_small_mw_kernel(const typename E::T *__restrict__ q, const typename E::T *__restrict__ k,
+                      const typename E::T *__restrict__ v, typename E::T *__restrict__ o,
+                      SmallArgs a)
+{
+    static_assert(GRID != kGridAny, "the fixed 8 x 8 grids keep a patch inside a token tile");
+    constexpr int N = 64;
+    using L = MwLds<E, D>;
+    constexpr int NCT = L::NCT;
+    constexpr bool PAD = D % 16 != 0;
+    extern __shared__ __attribute__((aligned(16))) float lds[];
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+    const int g = lane >> 4, c = lane & 15;
+    const int m = GRID == kGrid2x2 ? 16 : 8;
+    float *vec = lds + L::vec + 64 * w;
+    const int64_t base = int64_t(blockIdx.x) * N * D;
+    const typename E::T *qu = q + base, *ku = k + base, *vu = v + base;
+    typename E::T *ou = o + base;
+
+    // ---- loads of this wave's token tile w
+    const int off = (16 * w + c) * D + chunk_start<D>(g);
+    float qr[8], kr[8];
+    bf8 qw, kw;
+    if constexpr (BFM) {
+        qw = load_row8_bf16(reinterpret_cast<const uint16_t *>(qu) + off);
+        kw = load_row8_bf16(reinterpret_cast<const uint16_t *>(ku) + off);
+    } else {
+        load_row8<D>(qu + off, qr);
+        load_row8<D>(ku + off, kr);
+    }
+    // V rows 16w+4g+s of column 16ct+c (the ones column at column D)
+    float vr[NCT][4];
+    uint16_t vh[NCT][4];
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) {
+        const int f = 16 * ct + c;
+        const int vlane = (16 * w + 4 * g) * D + min(f, D - 1);
+        const bool ones = PAD && ct == NCT - 1 && f == D;
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+            if constexpr (BFM) {
+                const uint16_t y = reinterpret_cast<const uint16_t *>(vu)[vlane + x * D];
+                vh[ct][x] = ones ? uint16_t(0x3F80) : y;
+            } else {
+                const float y = E::load(vu, vlane + x * D);
+                vr[ct][x] = ones ? 1.f : y;
+            }
+        }
+    }
+
+    // ---- Step 1: every wave stages its rows; every wave forms the patch sums.
+    float qb[8], kb[8];
+    if constexpr (BFM) {
+        stage_chunk<E>(qw, lds + L::qst, w, g, c);
+        stage_chunk<E>(kw, lds + L::kst, w, g, c);
+    } else {
+        stage_chunk<E>(qr, lds + L::qst, w, g, c);
+        stage_chunk<E>(kr, lds + L::kst, w, g, c);
+    }
+    __syncthreads();
+    patch_sums<E, D, GRID>(lds + L::qst, qb, m, g, c);
+    patch_sums<E, D, GRID>(lds + L::kst, kb, m, g, c);
+    bf8 kbh, kbl, qbh, qbl;
+    if constexpr (BFM) {
+        split_bf16(kb, kbh, kbl);
+        split_bf16(qb, qbh, qbl);
+    }
+    const float s2u = a.s2 * a.inv_patch;    // one pooled side (S_L, S_U)
+    const float s2a = s2u * a.inv_patch;     // both sides pooled (S_A)
+
+    // ---- Step 3, G_U side over this wave's keys; the row maxima over all
+    // keys come from the four waves' maxima.
+    f4 su = {0.f, 0.f, 0.f, 0.f};   // lane (g,c): S_U[landmark c][key 16w+4g+i]
+    if constexpr (BFM) {
+        su = mfma_bf16(kw, qbh, su);
+        su = mfma_bf16(kw, qbl, su);
+    } else {
+#pragma unroll
+        for (int x = 0; x < 8; ++x)
+            su = mfma4(kr[x], qb[x], su);
+    }
+    {
+        const float mw = max_groups(fmaxf(fmaxf(su[0], su[1]), fmaxf(su[2], su[3])));
+        if (g == 0)
+            lds[L::xm + 16 * w + c] = mw;
+    }
+    // ---- Step 3, G_L side for this wave's query tile (no exchange needed).
+    // glT lane (g,c): G_L^n[token 16w+c][landmark 4g+i].
+    f4 glT;
+    {
+        f4 acc = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (BFM) {
+            acc = mfma_bf16(kbh, qw, acc);
+            acc = mfma_bf16(kbl, qw, acc);
+        } else {
+#pragma unroll
+            for (int x = 0; x < 8; ++x)
+                acc = mfma4(kb[x], qr[x], acc);
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (4 * g + i < m)
+                mx = fmaxf(mx, acc[i]);
+        mx = s2u * max_groups(mx);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            glT[i] = (4 * g + i < m) ? fast_exp2(fmaf(s2u, acc[i], -mx)) : 0.f;
+    }
+    __syncthreads();   // the waves' maxima
+    float mu = lds[L::xm + c];
+#pragma unroll
+    for (int u = 1; u < 4; ++u)
+        mu = fmaxf(mu, lds[L::xm + 16 * u + c]);
+    mu *= s2u;   // m_U of landmark c (base-2 units)
+    float tden = 0.f;
+    f4 e;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        e[i] = (c < m) ? fast_exp2(fmaf(s2u, su[i], -mu)) : 0.f;
+        tden += e[i];
+    }
+    // T_w = G_U^n [V | 1] over this wave's 16 keys: T[ct] lane (g,c) holds
+    // T_w[landmark 4g+i][column 16ct+c].
+    f4 T[NCT];
+    if constexpr (BFM) {
+        // the bf16 product contracts 32 keys: this tile's, then 16 zeros
+        float g8[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            g8[i] = e[i];
+            g8[4 + i] = 0.f;
+        }
+        bf8 gh, gl;
+        split_bf16(g8, gh, gl);
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct) {
+            const uint16_t v8[8] = {vh[ct][0], vh[ct][1], vh[ct][2], vh[ct][3], 0, 0, 0, 0};
+            const bf8 vv = pack_bf8(v8);
+            T[ct] = mfma_bf16(gh, vv, f4{0.f, 0.f, 0.f, 0.f});
+            T[ct] = mfma_bf16(gl, vv, T[ct]);
+        }
+    } else {
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct) {
+            f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+                acc = mfma4(e[x], vr[ct][x], acc);
+            T[ct] = acc;
+        }
+    }
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct)
+        reinterpret_cast<f4 *>(lds + L::xt + (w * NCT + ct) * 256)[lane] = T[ct];
+    if constexpr (!PAD) {
+        tden = sum_groups(tden);
+        if (g == 0)
+            lds[L::xd + 16 * w + c] = tden;
+    }
+    __syncthreads();   // the waves' partial sums
+
+    if (w == 0) {
+        // T and T_D of the unit: the four waves' sums, in wave order.
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct) {
+            f4 acc = reinterpret_cast<const f4 *>(lds + L::xt + ct * 256)[lane];
+#pragma unroll
+            for (int u = 1; u < 4; ++u)
+                acc += reinterpret_cast<const f4 *>(lds + L::xt + (u * NCT + ct) * 256)[lane];
+            T[ct] = acc;
+        }
+        if constexpr (!PAD)
+            tden = lds[L::xd + c] + lds[L::xd + 16 + c] + lds[L::xd + 32 + c] +
+                   lds[L::xd + 48 + c];
+        float *scr = lds + L::scr;
+        // ---- Step 2: G_A^n.  AT lane (g,c): A[c][4g+i].
+        f4 AT;
+        {
+            f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int x = 0; x < 8; ++x)
+                acc = mfma4(kb[x], qb[x], acc);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                AT[i] = (c < m && 4 * g + i < m) ? fast_exp2(fmaf(s2a, acc[i], -mu)) : 0.f;
+        }
+        // ---- Step 4, as in the one-wave kernel.
+        const float rowsum = sum_groups(AT[0] + AT[1] + AT[2] + AT[3]);
+        const float colsum = fmaxf(fmaxf(sum_row(AT[0]), sum_row(AT[1])),
+                                   fmaxf(sum_row(AT[2]), sum_row(AT[3])));
+        const float norm_inf = max_groups(max_row(rowsum));
+        const float norm_1 = max_groups(colsum);
+        const float alpha = 1.0f / (norm_1 * norm_inf);
+        const f4 A = transpose16(AT, scr, g, c);
+        f4 Z = AT * alpha, ZT = A * alpha;
+        f4 eye;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            eye[i] = (4 * g + i == c && c < m) ? 1.f : 0.f;
+        const f4 ATq = AT * 0.25f, e28 = eye * 28.f, e15 = eye * 15.f, e13q = eye * 3.25f;
+        if constexpr (BFM) {
+            const SplitPair Aq = both_orders(split_tile(ATq).hl);
+            auto step = [&]() {
+                const bf8 zs = split_tile(Z).hl;
+                const SplitPair ZTs = transpose_split(zs, scr, g, c);
+                const f4 Xq = mm16_hl(Aq, zs);
+                const bf8 xs = split_tile(Xq).hl;
+                const SplitPair XTq = transpose_split(xs, scr, g, c);
+                const f4 X2 = mm16_hl(XTq, xs);
+                f4 Y;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    Y[i] = fmaf(X2[i], 16.f, fmaf(Xq[i], -28.f, e15[i]));
+                Y = e13q - mm16_hl(XTq, split_tile(Y).hl);
+                Z = mm16_hl(ZTs, split_tile(Y).hl);
+            };
+            if constexpr (KF > 0) {
+#pragma unroll
+                for (int it = 0; it < KF; ++it)
+                    step();
+            } else {
+                for (int it = 0; it < a.iters; ++it)
+                    step();
+            }
+            if (KF > 0 || a.iters > 0)
+                ZT = transpose16(Z, scr, g, c);
+        } else {
+            auto step = [&]() {
+                const f4 Xq = mm16(ATq, Z);
+                const f4 XTq = transpose16(Xq, scr, g, c);
+                f4 Y;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    Y[i] = fmaf(Xq[i], -16.f, e28[i]);
+                Y = e15 - mm16(XTq, Y);
+                Y = e13q - mm16(XTq, Y);
+                Z = mm16(ZT, Y);
+                ZT = transpose16(Z, scr, g, c);
+            };
+            if constexpr (KF > 0) {
+#pragma unroll
+                for (int it = 0; it < KF; ++it)
+                    step();
+            } else {
+                for (int it = 0; it < a.iters; ++it)
+                    step();
+            }
+        }
+        // ---- Steps 5-6 re-associated: W = Z T, published for every wave.
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct)
+            reinterpret_cast<f4 *>(lds + L::wt + ct * 256)[lane] = mm16(ZT, T[ct]);
+        if constexpr (!PAD) {
+            const f4 td = by_rows(tden, vec, g, c);
+            const float wden =
+                sum_groups(ZT[0] * td[0] + ZT[1] * td[1] + ZT[2] * td[2] + ZT[3] * td[3]);
+            reinterpret_cast<f4 *>(lds + L::wt + NCT * 256)[lane] = by_rows(wden, vec, g, c);
+        }
+    }
+    __syncthreads();   // W
+
+    // ---- Steps 3 (G_L side), 6 and 7 for this wave's tile.
+    f4 Wt[NCT];
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct)
+        Wt[ct] = reinterpret_cast<const f4 *>(lds + L::wt + ct * 256)[lane];
+    f4 on[NCT];
+    if constexpr (BFM) {
+        const bf8 gs = split_tile(glT).hl;
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct)
+            on[ct] = mm16_lh(gs, both_orders(split_tile(Wt[ct]).hl));
+    } else {
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct)
+            on[ct] = mm16(glT, Wt[ct]);
+    }
+    f4 rcp;   // 1 / O_D[16w+4g+i]
+    if constexpr (PAD) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            rcp[i] = __builtin_amdgcn_rcpf(row_bcast<D % 16>(on[NCT - 1][i]));
+    } else {
+        const f4 wd = reinterpret_cast<const f4 *>(lds + L::wt + NCT * 256)[lane];
+        const float od = sum_groups(glT[0] * wd[0] + glT[1] * wd[1] + glT[2] * wd[2] +
+                                    glT[3] * wd[3]);
+        const f4 odr = by_rows(od, vec, g, c);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            rcp[i] = __builtin_amdgcn_rcpf(odr[i]);
+    }
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) {
+        const int f = 16 * ct + c;
+        if (f < D) {
+            f4 x;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                x[i] = on[ct][i] * rcp[i];
+            if constexpr (BFM) {
+                const uint32_t p01 = pack_bf16x2(x[0], x[1]), p23 = pack_bf16x2(x[2], x[3]);
+                uint16_t *dst = reinterpret_cast<uint16_t *>(ou) + (16 * w + 4 * g) * D + f;
+                dst[0] = uint16_t(p01);
+                dst[D] = uint16_t(p01 >> 16);
+                dst[2 * D] = uint16_t(p23);
+                dst[3 * D] = uint16_t(p23 >> 16);
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    ou[(16 * w + 4 * g + i) * D + f] = x[i];
+            }
+        }
+    }
+}
+
 bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
 
 int ilog2(int x)
@@ -607,6 +967,18 @@ constexpr int64_t kFewUnits = 4 * 256;
 template <class E, int NT, int D, int GRID = kGridAny, int KF = 0>
 void launch_small(const Problem &p, const SmallArgs &a, hipStream_t stream)
 {
+    if constexpr (NT == 4 && GRID != kGridAny) {
+        if (p.units < kFewUnits) {   // one unit per four-wave workgroup
+            const size_t lds = size_t(MwLds<E, D>::total) * sizeof(float);
+            hipLaunchKernelGGL((tiled_small_mw_kernel<E, D, E::bytes == 2, GRID, KF>),
+                               dim3(unsigned(p.units)), dim3(256), lds, stream,
+                               static_cast<const typename E::T *>(p.q),
+                               static_cast<const typename E::T *>(p.k),
+                               static_cast<const typename E::T *>(p.v),
+                               static_cast<typename E::T *>(p.o), a);
+            return;
+        }
+    }
     const int wpb = p.units < kFewUnits ? 1 : kWavesPerBlock;
     const unsigned blocks = unsigned((p.units + wpb - 1) / wpb);
     const size_t lds = size_t(wpb) * SmallLds<E, NT, D, GRID>::kPerWave * sizeof(float);
