@@ -234,6 +234,269 @@ exact_tiled_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         }
 }
 
+// ---- bf16, N a multiple of 64: key blocks streamed through LDS -------------
+//
+// A workgroup of NW waves covers 16 QT NW queries of one unit; wave w owns QT
+// query tiles and keeps their output, transposed, in registers.  The unit's
+// keys are streamed in blocks of 64 through two LDS buffers -- K rows, and V
+// transposed -- so every key and value is read from memory once per
+// workgroup; the next block is requested before the current one is computed.
+// Per block and query tile: S^T = K Q^T (one 16x16x32 bf16 product per key
+// tile), probabilities exp(s q.k - m) rounded to bf16 for O^T += V^T P^T (as
+// bf16 flash attention does), the row sums accumulated in fp32 from the
+// unrounded probabilities.
+//
+// The reference point m of a query's exponentials only grows, and only when a
+// score exceeds it by more than 2^8 (base 2): then it becomes the running
+// maximum over the four lane groups and the accumulated sums are rescaled.
+// Every probability thus stays in (0, 2^8], and the quotient of Eq. (1) is
+// the same for any reference point; only the rounding differs, and the bf16
+// rounding of a probability stays relative (at most 2^-8 of it).
+
+constexpr int kXB = 64;         // keys per block
+constexpr int kXKP = 40;        // pitch (bf16) of the K rows in LDS
+constexpr int kXVP = kXB + 8;   // pitch (bf16) of the V^T rows in LDS
+
+template <int D>
+struct XBufs {
+    static constexpr int kbytes = kXB * kXKP * 2;
+    static constexpr int vbytes = 32 * kXVP * 2;
+    static constexpr int bytes = kbytes + vbytes;   // one buffer
+};
+
+template <int D, int QT>
+__global__ void __launch_bounds__(512)
+exact_blocked_kernel(const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
+                     const uint16_t *__restrict__ v, uint16_t *__restrict__ o, int N, float s2,
+                     int wpu)
+{
+    constexpr int NCT = (D + 15) / 16;
+    using X = XBufs<D>;
+    extern __shared__ __attribute__((aligned(16))) unsigned char xsm[];
+    const int nw = blockDim.x >> 6;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+    const int g = lane >> 4, c = lane & 15;
+    const int64_t unit = blockIdx.x / wpu;
+    const int wg = int(blockIdx.x - unit * wpu);
+    const int64_t base = unit * int64_t(N) * D;
+    const uint16_t *qu = q + base, *ku = k + base, *vu = v + base;
+    uint16_t *ou = o + base;
+    const int q0 = (wg * nw + w) * 16 * QT;   // first query of this wave
+
+    // V^T rows past D are zero (both buffers, never overwritten by the
+    // staging below).  The row sums are fp32 sums of the unrounded
+    // probabilities, as in the one-row reference, not a ones column of V
+    // (which would sum the bf16-rounded ones).
+    if constexpr (16 * NCT > D) {
+        constexpr int kPad = (16 * NCT - D) * kXB;
+        for (int idx = threadIdx.x; idx < 2 * kPad; idx += blockDim.x) {
+            const int b = idx / kPad, r = idx % kPad;
+            const int f = D + r / kXB, key = r % kXB;
+            uint16_t *vt = reinterpret_cast<uint16_t *>(xsm + b * X::bytes + X::kbytes);
+            vt[f * kXVP + key] = uint16_t(0);
+        }
+    }
+    // Staging: thread t of the first 256 (a workgroup has at least four
+    // waves) takes key t / 4 of the block, chunk t % 4 (the slot layout of
+    // load_chunk8), of both K and V.
+    const bool stager = threadIdx.x < 256;
+    const int skey = (threadIdx.x >> 2) & 63, sg = threadIdx.x & 3;
+    U16B kst, vst;
+    auto fetch = [&](int blk) {
+        if (stager) {
+            const int64_t row = int64_t(blk * kXB + skey) * D + chunk_start<D>(sg);
+            kst = *reinterpret_cast<const U16B *>(ku + row);
+            vst = *reinterpret_cast<const U16B *>(vu + row);
+        }
+    };
+    auto store = [&](int buf) {
+        if (stager) {
+            unsigned char *bb = xsm + buf * X::bytes;
+            U16B kk = kst;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (!slot_valid<D>(sg, 2 * j))
+                    kk.w[j] = 0u;
+            *reinterpret_cast<U16B *>(bb + (skey * kXKP + 8 * sg) * 2) = kk;
+            uint16_t *vt = reinterpret_cast<uint16_t *>(bb + X::kbytes);
+#pragma unroll
+            for (int x = 0; x < 8; ++x)
+                if (slot_valid<D>(sg, x))
+                    vt[(chunk_start<D>(sg) + x) * kXVP + skey] =
+                        uint16_t(vst.w[x >> 1] >> (16 * (x & 1)));
+        }
+    };
+
+    // This wave's query tiles in the slot layout, raw bf16.
+    bf8 qf[QT];
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+        U16B u = *reinterpret_cast<const U16B *>(qu + int64_t(q0 + 16 * t + c) * D +
+                                                 chunk_start<D>(g));
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (!slot_valid<D>(g, 2 * j))
+                u.w[j] = 0u;
+        qf[t] = __builtin_bit_cast(bf8, u);
+    }
+    f4 OT[QT][NCT];   // O^T[feature 16ct+4g+i][query q0+16t+c]
+    float mref[QT], lsum[QT];
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct)
+            OT[t][ct] = f4{0.f, 0.f, 0.f, 0.f};
+        mref[t] = -INFINITY;
+        lsum[t] = 0.f;
+    }
+
+    const int nblk = N / kXB;
+    fetch(0);
+    store(0);
+    __syncthreads();
+    for (int blk = 0; blk < nblk; ++blk) {
+        const int buf = blk & 1;
+        if (blk + 1 < nblk)
+            fetch(blk + 1);   // in flight while this block is computed
+        const unsigned char *bb = xsm + buf * X::bytes;
+        bf8 kf[4];
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+            kf[kt] = *reinterpret_cast<const bf8 *>(bb + ((16 * kt + c) * kXKP + 8 * g) * 2);
+        // A operands of the value product: V^T rows 16ct+c, keys {4g..4g+3}
+        // of the tiles 2kp and 2kp+1 (the k order of the probabilities below).
+        bf8 vf[2][NCT];
+        const uint16_t *vt = reinterpret_cast<const uint16_t *>(bb + X::kbytes);
+#pragma unroll
+        for (int kp = 0; kp < 2; ++kp)
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) {
+                const uint16_t *row = vt + (16 * ct + c) * kXVP + 32 * kp + 4 * g;
+                const uint2 a0 = *reinterpret_cast<const uint2 *>(row);
+                const uint2 a1 = *reinterpret_cast<const uint2 *>(row + 16);
+                U16B u;
+                u.w[0] = a0.x; u.w[1] = a0.y; u.w[2] = a1.x; u.w[3] = a1.y;
+                vf[kp][ct] = __builtin_bit_cast(bf8, u);
+            }
+#pragma unroll
+        for (int t = 0; t < QT; ++t) {
+            f4 st[4];   // lane (g,c): S^T[key 16kt+4g+i][query q0+16t+c]
+            float lmax = -INFINITY;
+#pragma unroll
+            for (int kt = 0; kt < 4; ++kt) {
+                st[kt] = mfma_bf16(kf[kt], qf[t], f4{0.f, 0.f, 0.f, 0.f});
+                lmax = fmaxf(lmax, fmaxf(fmaxf(st[kt][0], st[kt][1]), fmaxf(st[kt][2], st[kt][3])));
+            }
+            if (__builtin_amdgcn_ballot_w64(s2 * lmax > mref[t] + 8.f) != 0) {
+                const float mnew = fmaxf(mref[t], s2 * max_groups(lmax));
+                const float f = fast_exp2(mref[t] - mnew);   // 0 on the first block
+                lsum[t] *= f;
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct)
+                    OT[t][ct] *= f;
+                mref[t] = mnew;
+            }
+#pragma unroll
+            for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    st[kt][i] = fast_exp2(fmaf(s2, st[kt][i], -mref[t]));
+                    lsum[t] += st[kt][i];
+                }
+#pragma unroll
+            for (int kp = 0; kp < 2; ++kp) {
+                U16B pb;
+                pb.w[0] = cvt_bf16x2(st[2 * kp][0], st[2 * kp][1]);
+                pb.w[1] = cvt_bf16x2(st[2 * kp][2], st[2 * kp][3]);
+                pb.w[2] = cvt_bf16x2(st[2 * kp + 1][0], st[2 * kp + 1][1]);
+                pb.w[3] = cvt_bf16x2(st[2 * kp + 1][2], st[2 * kp + 1][3]);
+                const bf8 pv = __builtin_bit_cast(bf8, pb);
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct)
+                    OT[t][ct] = mfma_bf16(vf[kp][ct], pv, OT[t][ct]);
+            }
+        }
+        if (blk + 1 < nblk)
+            store(buf ^ 1);
+        __syncthreads();
+    }
+
+    // Divide by the row sums and store rows of O.
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+        const float inv = __builtin_amdgcn_rcpf(sum_groups(lsum[t]));
+        uint16_t *orow = ou + int64_t(q0 + 16 * t + c) * D;
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct) {
+            const int f = 16 * ct + 4 * g;
+            const uint32_t p01 = cvt_bf16x2(OT[t][ct][0] * inv, OT[t][ct][1] * inv);
+            const uint32_t p23 = cvt_bf16x2(OT[t][ct][2] * inv, OT[t][ct][3] * inv);
+            if (f + 1 < D)
+                *reinterpret_cast<uint32_t *>(orow + f) = p01;
+            if (f + 3 < D)
+                *reinterpret_cast<uint32_t *>(orow + f + 2) = p23;
+        }
+    }
+}
+
+// Query tiles per wave (four from 256 tokens on, so that a K or V fragment
+// read from LDS serves four products; one below, so that a workgroup still
+// has four waves to stage a block) and waves per workgroup.
+constexpr int kXMaxWaves = 8;
+inline int exact_qt(int N) { return N >= 256 ? 4 : 1; }
+
+bool exact_blocked_ok(const Problem &p)
+{
+    if (p.dtype != 1 || p.N % kXB != 0 || !tiled_width(p.d) || p.d % 2 != 0)
+        return false;
+    const uintptr_t mis = uintptr_t(p.q) | uintptr_t(p.k) | uintptr_t(p.v) | uintptr_t(p.o);
+    if (mis % 4 != 0)
+        return false;
+    // whole-wave query groups that divide evenly into workgroups of at least
+    // four waves, and the grid under 2^32 work-items
+    const int tiles = p.N / (16 * exact_qt(p.N));
+    const int nw = tiles < kXMaxWaves ? tiles : kXMaxWaves;
+    if (nw < 4 || tiles % nw != 0)
+        return false;
+    return p.units * int64_t(p.N) * 64 / (16 * exact_qt(p.N)) < (int64_t(1) << 32);
+}
+
+template <int D, int QT>
+void launch_exact_blocked_qt(const Problem &p, hipStream_t stream)
+{
+    const int tiles = p.N / (16 * QT);              // wave-sized query groups per unit
+    const int nw = tiles < kXMaxWaves ? tiles : kXMaxWaves;
+    const int wpu = tiles / nw;
+    const size_t lds = 2 * size_t(XBufs<D>::bytes);
+    hipLaunchKernelGGL((exact_blocked_kernel<D, QT>), dim3(unsigned(p.units * wpu)),
+                       dim3(64 * nw), lds, stream, static_cast<const uint16_t *>(p.q),
+                       static_cast<const uint16_t *>(p.k), static_cast<const uint16_t *>(p.v),
+                       static_cast<uint16_t *>(p.o), p.N, p.scale * kLog2e, wpu);
+}
+
+template <int D>
+void launch_exact_blocked(const Problem &p, hipStream_t stream)
+{
+    if (exact_qt(p.N) == 4)
+        launch_exact_blocked_qt<D, 4>(p, stream);
+    else
+        launch_exact_blocked_qt<D, 1>(p, stream);
+}
+
+void launch_exact_blocked_d(const Problem &p, hipStream_t stream)
+{
+    switch (p.d) {
+    case 8: launch_exact_blocked<8>(p, stream); break;
+    case 12: launch_exact_blocked<12>(p, stream); break;
+    case 16: launch_exact_blocked<16>(p, stream); break;
+    case 20: launch_exact_blocked<20>(p, stream); break;
+    case 24: launch_exact_blocked<24>(p, stream); break;
+    case 28: launch_exact_blocked<28>(p, stream); break;
+    case 30: launch_exact_blocked<30>(p, stream); break;
+    default: launch_exact_blocked<32>(p, stream); break;
+    }
+}
+
 // V^T of one unit in LDS for the bf16 path; larger windows run the fp32
 // matrix cores on the (exactly converted) bf16 inputs instead.
 constexpr size_t kExactLdsMax = 128 * 1024;
@@ -291,6 +554,10 @@ bool exact_tiled_ok(const Problem &p)
 template <class E>
 hipError_t launch_exact_t(const Problem &p, hipStream_t stream)
 {
+    if (exact_blocked_ok(p)) {
+        launch_exact_blocked_d(p, stream);
+        return hipGetLastError();
+    }
     if (exact_tiled_ok(p)) {
         launch_exact_tiled_e<E>(p, stream);
         return hipGetLastError();

@@ -190,19 +190,23 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             for (int ct = 0; ct < NCT; ++ct) {
                 const int f = 16 * ct + c;
                 // one address per row group; the four rows are immediate offsets
+                // (pointer first, then the row offsets: constant multiples of d
+                // that fold into the loads' immediate offsets)
                 const unsigned vrow = unsigned(16 * tt + 4 * g) * d + unsigned(min(f, d - 1));
+                const uint16_t *vp16 = vu16 + vrow;
+                const typename E::T *vp = vu + vrow;
                 if constexpr (BFM) {
 #pragma unroll
                     for (int pp = 0; pp < 2; ++pp) {
                         u16x2 pr;
-                        pr.x = vu16[vrow + 2 * pp * d];
-                        pr.y = vu16[vrow + (2 * pp + 1) * d];
+                        pr.x = vp16[2 * pp * d];
+                        pr.y = vp16[(2 * pp + 1) * d];
                         vh_[u][ct][pp] = __builtin_bit_cast(uint32_t, pr);
                     }
                 } else {
 #pragma unroll
                     for (int x = 0; x < 4; ++x)
-                        vr_[u][ct][x] = E::load(vu + vrow, x * d);
+                        vr_[u][ct][x] = E::load(vp, x * d);
                 }
             }
         }
