@@ -439,6 +439,166 @@ exact_blocked_kernel(const uint16_t *__restrict__ q, const uint16_t *__restrict_
     }
 }
 
+// ---- fp32, N a multiple of 64: the same blocked structure on the fp32 matrix
+// cores.  K rows and V^T are staged as fp32; S^T tiles are eight-step
+// 16x16x4 products over the feature slots (the slot layout of load_chunk8);
+// the probabilities stay fp32 and feed O^T += V^T P^T directly in the
+// D-layout, with V^T read as the transposed left operand.
+
+constexpr int kFKP = 36;        // pitch (floats) of the K rows in LDS
+constexpr int kFVP = kXB + 4;   // pitch (floats) of the V^T rows in LDS
+
+struct FBufs {
+    static constexpr int kbytes = kXB * kFKP * 4;
+    static constexpr int vbytes = 32 * kFVP * 4;
+    static constexpr int bytes = kbytes + vbytes;
+};
+
+template <int D, int QT>
+__global__ void __launch_bounds__(512)
+exact_blocked_f32_kernel(const float *__restrict__ q, const float *__restrict__ k,
+                         const float *__restrict__ v, float *__restrict__ o, int N, float s2,
+                         int wpu)
+{
+    constexpr int NCT = (D + 15) / 16;
+    using X = FBufs;
+    extern __shared__ __attribute__((aligned(16))) unsigned char xsm[];
+    const int nw = blockDim.x >> 6;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+    const int g = lane >> 4, c = lane & 15;
+    const int64_t unit = blockIdx.x / wpu;
+    const int wg = int(blockIdx.x - unit * wpu);
+    const int64_t base = unit * int64_t(N) * D;
+    const float *qu = q + base, *ku = k + base, *vu = v + base;
+    float *ou = o + base;
+    const int q0 = (wg * nw + w) * 16 * QT;
+
+    if constexpr (16 * NCT > D) {   // V^T rows past D are zero in both buffers
+        constexpr int kPad = (16 * NCT - D) * kXB;
+        for (int idx = threadIdx.x; idx < 2 * kPad; idx += blockDim.x) {
+            const int b = idx / kPad, r = idx % kPad;
+            float *vt = reinterpret_cast<float *>(xsm + b * X::bytes + X::kbytes);
+            vt[(D + r / kXB) * kFVP + r % kXB] = 0.f;
+        }
+    }
+    // Staging: thread t of the first 256 takes key t / 4, chunk t % 4.
+    const bool stager = threadIdx.x < 256;
+    const int skey = (threadIdx.x >> 2) & 63, sg = threadIdx.x & 3;
+    float kst[8], vst[8];
+    auto fetch = [&](int blk) {
+        if (stager) {
+            const int64_t row = int64_t(blk * kXB + skey) * D + chunk_start<D>(sg);
+            load_row8<D>(ku + row, kst);
+            load_row8<D>(vu + row, vst);
+        }
+    };
+    auto store = [&](int buf) {
+        if (stager) {
+            unsigned char *bb = xsm + buf * X::bytes;
+            float *krow = reinterpret_cast<float *>(bb) + skey * kFKP + 8 * sg;
+            f4 k0, k1;
+#pragma unroll
+            for (int x = 0; x < 4; ++x) {
+                k0[x] = slot_valid<D>(sg, x) ? kst[x] : 0.f;
+                k1[x] = slot_valid<D>(sg, 4 + x) ? kst[4 + x] : 0.f;
+            }
+            reinterpret_cast<f4 *>(krow)[0] = k0;
+            reinterpret_cast<f4 *>(krow)[1] = k1;
+            float *vt = reinterpret_cast<float *>(bb + X::kbytes);
+#pragma unroll
+            for (int x = 0; x < 8; ++x)
+                if (slot_valid<D>(sg, x))
+                    vt[(chunk_start<D>(sg) + x) * kFVP + skey] = vst[x];
+        }
+    };
+
+    float qf[QT][8];
+#pragma unroll
+    for (int t = 0; t < QT; ++t)
+        load_chunk8<F32, D>(qu + int64_t(q0 + 16 * t + c) * D, g, qf[t]);
+    f4 OT[QT][NCT];
+    float mref[QT], lsum[QT];
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct)
+            OT[t][ct] = f4{0.f, 0.f, 0.f, 0.f};
+        mref[t] = -INFINITY;
+        lsum[t] = 0.f;
+    }
+
+    const int nblk = N / kXB;
+    fetch(0);
+    store(0);
+    __syncthreads();
+    for (int blk = 0; blk < nblk; ++blk) {
+        const int buf = blk & 1;
+        if (blk + 1 < nblk)
+            fetch(blk + 1);
+        const unsigned char *bb = xsm + buf * X::bytes;
+        const float *kb = reinterpret_cast<const float *>(bb);
+        const float *vt = reinterpret_cast<const float *>(bb + X::kbytes);
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) {
+            float kf[8];   // K row 16kt+c, slots of group g
+            {
+                const f4 a0 = reinterpret_cast<const f4 *>(kb + (16 * kt + c) * kFKP + 8 * g)[0];
+                const f4 a1 = reinterpret_cast<const f4 *>(kb + (16 * kt + c) * kFKP + 8 * g)[1];
+#pragma unroll
+                for (int x = 0; x < 4; ++x) {
+                    kf[x] = a0[x];
+                    kf[4 + x] = a1[x];
+                }
+            }
+            f4 vl[NCT];   // V^T tile (ct, kt) as the left operand: lane (g,c) V[16kt+4g+i][16ct+c]
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct)
+                vl[ct] = *reinterpret_cast<const f4 *>(vt + (16 * ct + c) * kFVP + 16 * kt + 4 * g);
+#pragma unroll
+            for (int t = 0; t < QT; ++t) {
+                f4 st = {0.f, 0.f, 0.f, 0.f};   // S^T[key 16kt+4g+i][query q0+16t+c]
+#pragma unroll
+                for (int x = 0; x < 8; ++x)
+                    st = mfma4(kf[x], qf[t][x], st);
+                const float lmax = fmaxf(fmaxf(st[0], st[1]), fmaxf(st[2], st[3]));
+                if (__builtin_amdgcn_ballot_w64(s2 * lmax > mref[t] + 8.f) != 0) {
+                    const float mnew = fmaxf(mref[t], s2 * max_groups(lmax));
+                    const float f = fast_exp2(mref[t] - mnew);
+                    lsum[t] *= f;
+#pragma unroll
+                    for (int ct = 0; ct < NCT; ++ct)
+                        OT[t][ct] *= f;
+                    mref[t] = mnew;
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    st[i] = fast_exp2(fmaf(s2, st[i], -mref[t]));
+                    lsum[t] += st[i];
+                }
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct)
+                    OT[t][ct] = mm16_acc(vl[ct], st, OT[t][ct]);
+            }
+        }
+        if (blk + 1 < nblk)
+            store(buf ^ 1);
+        __syncthreads();
+    }
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+        const float inv = __builtin_amdgcn_rcpf(sum_groups(lsum[t]));
+        float *orow = ou + int64_t(q0 + 16 * t + c) * D;
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int f = 16 * ct + 4 * g + i;
+                if (f < D)
+                    orow[f] = OT[t][ct][i] * inv;
+            }
+    }
+}
+
 // Query tiles per wave (four from 256 tokens on, so that a K or V fragment
 // read from LDS serves four products; one below, so that a workgroup still
 // has four waves to stage a block) and waves per workgroup.
@@ -447,10 +607,11 @@ inline int exact_qt(int N) { return N >= 256 ? 4 : 1; }
 
 bool exact_blocked_ok(const Problem &p)
 {
-    if (p.dtype != 1 || p.N % kXB != 0 || !tiled_width(p.d) || p.d % 2 != 0)
+    if (p.N % kXB != 0 || !tiled_width(p.d) || p.d % 2 != 0)
         return false;
+    // bf16: 16-byte row pieces at even elements and paired output stores
     const uintptr_t mis = uintptr_t(p.q) | uintptr_t(p.k) | uintptr_t(p.v) | uintptr_t(p.o);
-    if (mis % 4 != 0)
+    if (p.dtype == 1 && mis % 4 != 0)
         return false;
     // whole-wave query groups that divide evenly into workgroups of at least
     // four waves, and the grid under 2^32 work-items
@@ -467,11 +628,19 @@ void launch_exact_blocked_qt(const Problem &p, hipStream_t stream)
     const int tiles = p.N / (16 * QT);              // wave-sized query groups per unit
     const int nw = tiles < kXMaxWaves ? tiles : kXMaxWaves;
     const int wpu = tiles / nw;
-    const size_t lds = 2 * size_t(XBufs<D>::bytes);
-    hipLaunchKernelGGL((exact_blocked_kernel<D, QT>), dim3(unsigned(p.units * wpu)),
-                       dim3(64 * nw), lds, stream, static_cast<const uint16_t *>(p.q),
-                       static_cast<const uint16_t *>(p.k), static_cast<const uint16_t *>(p.v),
-                       static_cast<uint16_t *>(p.o), p.N, p.scale * kLog2e, wpu);
+    if (p.dtype == 1) {
+        const size_t lds = 2 * size_t(XBufs<D>::bytes);
+        hipLaunchKernelGGL((exact_blocked_kernel<D, QT>), dim3(unsigned(p.units * wpu)),
+                           dim3(64 * nw), lds, stream, static_cast<const uint16_t *>(p.q),
+                           static_cast<const uint16_t *>(p.k), static_cast<const uint16_t *>(p.v),
+                           static_cast<uint16_t *>(p.o), p.N, p.scale * kLog2e, wpu);
+    } else {
+        const size_t lds = 2 * size_t(FBufs::bytes);
+        hipLaunchKernelGGL((exact_blocked_f32_kernel<D, QT>), dim3(unsigned(p.units * wpu)),
+                           dim3(64 * nw), lds, stream, static_cast<const float *>(p.q),
+                           static_cast<const float *>(p.k), static_cast<const float *>(p.v),
+                           static_cast<float *>(p.o), p.N, p.scale * kLog2e, wpu);
+    }
 }
 
 template <int D>
