@@ -23,15 +23,24 @@ template <int MT>
 struct LargeLds {
     static constexpr int M = 16 * MT;
     static constexpr int P = M + 4;    // pitch (floats) of fp32 m x m matrices
-    static constexpr int PB = M + 8;   // pitch (bf16 elements) of transposed bf16 matrices
+    // Pitch (bf16 elements) of the transposed bf16 matrices.  Rows 2 words
+    // (mod 4) apart keep the 8-byte operand reads of 16 lanes on distinct
+    // banks (a pitch of 4 words mod 8 puts lanes c and c + 8 of a row group
+    // on one bank pair: measured a third slower).  One landmark tile keeps
+    // M + 8, which the key-pass records need.
+    static constexpr int PB = MT == 1 ? M + 8 : M + 4;
     static constexpr int RS = M * PB;  // one matrix region (floats): fp32 [M][P] or bf16 hi+lo
     static constexpr int kbar = 0;
-    static constexpr int colpart = kbar + M * kTS;      // [MT][M] column-sum partials
-    static constexpr int rowmax = colpart + MT * M;     // [MT] row-sum maxima (padded)
-    static constexpr int zb = rowmax + 4;
+    static constexpr int zb = kbar + M * kTS;
     static constexpr int ya = zb + RS;
     static constexpr int yb = ya + RS;                  // also the own-row transpose scratch
-    static constexpr int vec = yb + RS;                 // [MT][64]
+    static constexpr int vec = yb + RS;                 // [MT][64] row vectors
+    // Z_0's column-sum partials [MT][M] and row-sum maxima [MT] (padded) share
+    // the row-vector region, which no wave uses between the key pass and the
+    // query pass.
+    static constexpr int vec_len = 64 * MT > MT * M + 4 ? 64 * MT : MT * M + 4;
+    static constexpr int colpart = vec;
+    static constexpr int rowmax = colpart + MT * M;
     // Before the landmark core runs, its matrix regions hold the key pass of
     // the one-pass large kernel: the Qbar table and one record per wave (T
     // rows of every landmark, pitch kRecP; T_D; running maxima).
@@ -39,12 +48,16 @@ struct LargeLds {
     static constexpr int rec_len = M * kRecP + 2 * M;
     static constexpr int qtab = zb;
     static constexpr int recs = qtab + M * kTS;
+    // After the iteration the T table starts at zb and the W table ends at
+    // vec (both may run into the dead middle region); otherwise they follow.
     static constexpr int tab_len = M * kTS + M;         // table + its denominator column
-    static constexpr bool tab_in_y = tab_len <= RS;     // T in ya, W in yb after the iteration
-    static constexpr int tb = tab_in_y ? ya : vec + MT * 64;
-    static constexpr int wb = tab_in_y ? yb : tb + tab_len;
-    static constexpr int total = tab_in_y ? vec + MT * 64 : wb + tab_len;
-    static_assert(recs + MT * rec_len <= vec, "key-pass records fit the core's regions");
+    static constexpr bool tab_in = 2 * tab_len <= 3 * RS;
+    static constexpr int tb = tab_in ? zb : vec + vec_len;
+    static constexpr int wb = tab_in ? vec - tab_len : tb + tab_len;
+    static constexpr int total = tab_in ? vec + vec_len : wb + tab_len;
+    static_assert(recs + MT * rec_len <= vec, "key-pass records fit the matrix regions");
+    static_assert((M - 1) * P + M <= RS, "the fp32 scratch fits its region");
+    static_assert(tb + tab_len <= wb, "the T and W tables do not overlap");
 };
 
 // Right-hand operand (D-layout) of tile (a, b) of a row-major LDS matrix.
@@ -81,14 +94,14 @@ __device__ inline void write_tile(float *B, int a, int b, f4 v, int g, int c)
 template <int M, int PB>
 __device__ inline void publish_bf(uint16_t *reg, int a, int b, f4 v, int g, int c)
 {
-    // Pairs converted together (round to nearest even), the hi terms widened
-    // back by a shift or a mask: the values of an element-wise split.
+    // Pairs converted together (round to nearest even): the values of an
+    // element-wise split.
+    const NegSel s = neg_selectors();
     uint32_t h[2], l[2];
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
         h[p] = cvt_bf16x2(v[2 * p], v[2 * p + 1]);
-        const float h0 = __uint_as_float(h[p] << 16), h1 = __uint_as_float(h[p] & 0xffff0000u);
-        l[p] = cvt_bf16x2(v[2 * p] - h0, v[2 * p + 1] - h1);
+        l[p] = residual_bf16x2(h[p], v[2 * p], v[2 * p + 1], s);
     }
     uint16_t *hp = reg + (16 * b + c) * PB + 16 * a + 4 * g;
     *reinterpret_cast<uint2 *>(hp) = make_uint2(h[0], h[1]);
@@ -305,6 +318,7 @@ __device__ inline void landmark_core(float *lds, const float (&qb)[8], float mu,
 #pragma unroll
     for (int j = 0; j < MT; ++j)
         ZLT[j] = read_lt<P>(Zb, lt, j, g, c);
+    __syncthreads();   // every wave has its Z_0 row (the T table may follow in Zb)
 
     // Iteration: X = A Z; Z <- Z (13I - X (15I - X (7I - X))) / 4, each wave
     // producing its row tile of every product.

@@ -79,17 +79,44 @@ __device__ inline uint32_t cvt_bf16x2(float lo, float hi)
     return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2{lo, hi}), b2));   // RNE
 }
 
+// The residuals x - hi of a converted pair, one v_dot2_f32_bf16 each:
+// x0 + (-1) hi0 + 0 hi1 and x1 + 0 hi0 + (-1) hi1.  Every partial result is
+// exact (hi is x rounded to 8 bits, so x - hi is an fp32 value), so these are
+// the values of the subtractions x - float(hi), without widening hi first.
+// The selectors (-1, 0) and (0, -1) come from SALU moves the compiler cannot
+// fold: as a literal, 0xbf800000 would be encoded as the fp32 inline
+// constant -1.0, which a packed bf16 operand does not read as (0, -1).
+struct NegSel {
+    uint32_t s0, s1;
+};
+
+__device__ inline NegSel neg_selectors()
+{
+    uint32_t a, b;
+    asm("s_mov_b32 %0, 0xbf80" : "=s"(a));
+    asm("s_mov_b32 %0, 0xbf800000" : "=s"(b));
+    return NegSel{a, b};
+}
+
+__device__ inline uint32_t residual_bf16x2(uint32_t h, float x0, float x1, NegSel s)
+{
+    typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+    const b2 hv = __builtin_bit_cast(b2, h);
+    const float l0 = __builtin_amdgcn_fdot2_f32_bf16(hv, __builtin_bit_cast(b2, s.s0), x0, false);
+    const float l1 = __builtin_amdgcn_fdot2_f32_bf16(hv, __builtin_bit_cast(b2, s.s1), x1, false);
+    return cvt_bf16x2(l0, l1);
+}
+
 // Eight fp32 values as hi = bf16(x) and lo = bf16(x - hi), both rounded to
 // nearest even, converted in pairs.
 __device__ inline void split_bf16(const float (&x)[8], bf8 &hi, bf8 &lo)
 {
+    const NegSel s = neg_selectors();
     U16B h, l;
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
         h.w[p] = cvt_bf16x2(x[2 * p], x[2 * p + 1]);
-        const float h0 = __uint_as_float(h.w[p] << 16);
-        const float h1 = __uint_as_float(h.w[p] & 0xffff0000u);
-        l.w[p] = cvt_bf16x2(x[2 * p] - h0, x[2 * p + 1] - h1);
+        l.w[p] = residual_bf16x2(h.w[p], x[2 * p], x[2 * p + 1], s);
     }
     hi = __builtin_bit_cast(bf8, h);
     lo = __builtin_bit_cast(bf8, l);
@@ -97,13 +124,12 @@ __device__ inline void split_bf16(const float (&x)[8], bf8 &hi, bf8 &lo)
 
 __device__ inline SplitTile split_tile(f4 x)
 {
+    const NegSel s = neg_selectors();
     U16B u;
     u.w[0] = cvt_bf16x2(x[0], x[1]);
     u.w[1] = cvt_bf16x2(x[2], x[3]);
-    const float h0 = __uint_as_float(u.w[0] << 16), h1 = __uint_as_float(u.w[0] & 0xffff0000u);
-    const float h2 = __uint_as_float(u.w[1] << 16), h3 = __uint_as_float(u.w[1] & 0xffff0000u);
-    u.w[2] = cvt_bf16x2(x[0] - h0, x[1] - h1);
-    u.w[3] = cvt_bf16x2(x[2] - h2, x[3] - h3);
+    u.w[2] = residual_bf16x2(u.w[0], x[0], x[1], s);
+    u.w[3] = residual_bf16x2(u.w[1], x[2], x[3], s);
     return SplitTile{__builtin_bit_cast(bf8, u)};
 }
 
