@@ -43,7 +43,7 @@
  *   (hipGetLastError) right before it launches, so an error left by an
  *   earlier, unrelated HIP call is not reported as its own.  Nothing throws
  *   or aborts across this boundary.
- * Limits.  1 <= N <= 2^20, 1 <= d_h <= 64, 1 <= m <= min(N, 64),
+ * Limits.  1 <= N <= 2^20, 1 <= d_h <= 128, 1 <= m <= min(N, 64),
  *   n_windows * heads <= 2^24 - 1 (every grid stays under 2^32 work-items),
  *   0 <= pinv_iters <= 64.  Pointers must be aligned to the element size.
  *   O must not overlap Q, K or V (Q, K, V may alias each other).
@@ -203,7 +203,7 @@ int nystra_attn_forward_noalloc(const void *Q, const void *K, const void *V, voi
  * attention output are stored in `dtype` in the workspace (as a model in that
  * dtype stores them); products accumulate in fp32 on the matrix cores.
  * Limits: window divides height and width, 0 <= shift < window, heads
- * divides channels, d_h <= 64, channels <= 4096, batch * height * width
+ * divides channels, d_h <= 128, channels <= 4096, batch * height * width
  * <= 2^31 - 1, and the attention limits above for N, m and the unit count.
  * nystra_block_workspace_size: host-only size of the workspace
  * nystra_block_forward needs (Q, K, V, O and, for long windows, the

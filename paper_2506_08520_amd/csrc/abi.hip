@@ -49,7 +49,7 @@ namespace {
 // Tokens per window: up to 2^20 (a 1024 x 1024 map as one global window).  The
 // kernels stream over tokens with 64-bit offsets and size LDS independently of N.
 constexpr int kMaxN = 1 << 20;
-constexpr int kMaxD = 64;
+constexpr int kMaxD = 128;
 constexpr int kMaxM = 64;
 constexpr int kMaxIters = 64;
 // Units per call: every kernel's grid is at most 256 work-items per unit in its

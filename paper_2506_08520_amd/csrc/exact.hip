@@ -18,17 +18,18 @@ namespace nystra {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kMaxD = 64;
-constexpr int kKeyTile = 64;   // keys staged in LDS per step
 
 // One thread per query row; keys and values of the unit are staged through
-// LDS in tiles of kKeyTile rows shared by the whole workgroup.
-template <class E>
+// LDS in tiles of kKeyTile rows shared by the whole workgroup.  DM bounds d_h
+// (64 or 128; the per-thread rows are sized by it).
+template <class E, int DM>
 __global__ void __launch_bounds__(kThreads)
 exact_rows_kernel(const typename E::T *__restrict__ q, const typename E::T *__restrict__ k,
                   const typename E::T *__restrict__ v, typename E::T *__restrict__ o,
                   int N, int d, float scale)
 {
+    constexpr int kMaxD = DM;
+    constexpr int kKeyTile = 4096 / DM;   // keys staged in LDS per step (32 KB)
     __shared__ float ks[kKeyTile * kMaxD];
     __shared__ float vs[kKeyTile * kMaxD];
     const int64_t base = int64_t(blockIdx.x) * N * d;
@@ -732,11 +733,16 @@ hipError_t launch_exact_t(const Problem &p, hipStream_t stream)
         return hipGetLastError();
     }
     const dim3 grid(unsigned(p.units), unsigned((p.N + kThreads - 1) / kThreads));
-    hipLaunchKernelGGL(exact_rows_kernel<E>, grid, dim3(kThreads), 0, stream,
-                       static_cast<const typename E::T *>(p.q),
-                       static_cast<const typename E::T *>(p.k),
-                       static_cast<const typename E::T *>(p.v),
-                       static_cast<typename E::T *>(p.o), p.N, p.d, p.scale);
+    const auto *q = static_cast<const typename E::T *>(p.q);
+    const auto *k = static_cast<const typename E::T *>(p.k);
+    const auto *v = static_cast<const typename E::T *>(p.v);
+    auto *o = static_cast<typename E::T *>(p.o);
+    if (p.d <= 64)
+        hipLaunchKernelGGL((exact_rows_kernel<E, 64>), grid, dim3(kThreads), 0, stream, q, k, v,
+                           o, p.N, p.d, p.scale);
+    else
+        hipLaunchKernelGGL((exact_rows_kernel<E, 128>), grid, dim3(kThreads), 0, stream, q, k,
+                           v, o, p.N, p.d, p.scale);
     return hipGetLastError();
 }
 

@@ -1,5 +1,5 @@
 // Portable PnP-Nystra kernels: one 256-thread workgroup per (window, head)
-// unit, every shape within the library limits (N <= 2^20, d_h <= 64, m <= 64),
+// unit, every shape within the library limits (N <= 2^20, d_h <= 128, m <= 64),
 // fp32 vector arithmetic, LDS for the small per-unit matrices.  They are the
 // fallback behind the MFMA-tiled kernels and the reference the tiled kernels
 // are compared against on shapes both cover.
@@ -11,7 +11,6 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-constexpr int kMaxD = 64;
 
 // Step 1 (Sec. 2.2): mean of the tokens of landmark l's pooling patch, for
 // every (l, c) pair handled by this thread.  Writes fp32 [m][d] to dst.
@@ -50,22 +49,28 @@ landmark_pool_kernel(const typename E::T *__restrict__ q, const typename E::T *_
     }
 }
 
-// LDS carve-up of the generic forward kernel (floats).
+// LDS carve-up of the generic forward kernel (floats).  Qbar and m_U are
+// dead once A is formed, so Z, X, Y and Y2 take their place; W = Z T is
+// written over X, Y and Y2 after the iteration (or past them when it is
+// longer).  At m = 64, d_h = 128 the workgroup takes 148 KB.
 struct Lds {
     int kbar, qbar, mu, t, w, a, z, x, y, y2, norms, total;
     __host__ __device__ Lds(int m, int d)
     {
         int o = 0;
         kbar = o; o += m * d;
-        qbar = o; o += m * d;
-        mu = o;   o += m;
         t = o;    o += m * (d + 1);
-        w = o;    o += m * (d + 1);
         a = o;    o += m * m;
-        z = o;    o += m * m;
-        x = o;    o += m * m;
-        y = o;    o += m * m;
-        y2 = o;   o += m * m;
+        const int r = o;   // Qbar and m_U, then Z, X, Y, Y2 and W
+        qbar = r;
+        mu = r + m * d;
+        z = r;
+        x = z + m * m;
+        y = x + m * m;
+        y2 = y + m * m;
+        w = x;
+        const int wend = w + m * (d + 1), yend = y2 + m * m;
+        o = wend > yend ? wend : yend;
         norms = o; o += 2 * m + 1;
         total = o;
     }
@@ -92,7 +97,8 @@ __device__ void shift_neg(const float *src, float *dst, int m, float c)
     }
 }
 
-template <class E>
+// DM bounds d_h (64 or 128): the per-thread feature arrays are sized by it.
+template <class E, int DM>
 __global__ void __launch_bounds__(kThreads)
 generic_forward_kernel(const typename E::T *__restrict__ q, const typename E::T *__restrict__ k,
                        const typename E::T *__restrict__ v, typename E::T *__restrict__ o,
@@ -111,6 +117,7 @@ generic_forward_kernel(const typename E::T *__restrict__ q, const typename E::T 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const float s2 = scale * kLog2e;   // logits carried in base-2 units
 
+    constexpr int kMaxD = DM;
     // Step 1: landmarks.
     pool_unit<E>(qu, qbar, g, m, d, tid, kThreads);
     pool_unit<E>(ku, kbar, g, m, d, tid, kThreads);
@@ -165,7 +172,7 @@ generic_forward_kernel(const typename E::T *__restrict__ q, const typename E::T 
             acc = fmaf(qbar[i * d + c], kbar[j * d + c], acc);
         A[idx] = exp2f(acc * s2 - mu[i]);
     }
-    __syncthreads();
+    __syncthreads();   // Qbar and m_U dead from here (Z, X, Y, Y2 take their place)
 
     // Step 4: Z_0 = A^T / (||A||_1 ||A||_inf), then the iteration.
     for (int i = tid; i < m; i += kThreads) {
@@ -257,12 +264,12 @@ generic_forward_kernel(const typename E::T *__restrict__ q, const typename E::T 
     }
 }
 
-template <class E>
+template <class E, int DM>
 hipError_t launch_generic_t(const Problem &p, hipStream_t stream)
 {
     const Lds L(p.m, p.d);
     const size_t lds_bytes = size_t(L.total) * sizeof(float);
-    hipLaunchKernelGGL(generic_forward_kernel<E>, dim3(unsigned(p.units)), dim3(kThreads),
+    hipLaunchKernelGGL((generic_forward_kernel<E, DM>), dim3(unsigned(p.units)), dim3(kThreads),
                        lds_bytes, stream, static_cast<const typename E::T *>(p.q),
                        static_cast<const typename E::T *>(p.k),
                        static_cast<const typename E::T *>(p.v),
@@ -277,7 +284,11 @@ size_t generic_lds_bytes(int m, int d) { return size_t(Lds(m, d).total) * sizeof
 
 hipError_t launch_generic_forward(const Problem &p, hipStream_t stream)
 {
-    return p.dtype == 0 ? launch_generic_t<F32>(p, stream) : launch_generic_t<BF16>(p, stream);
+    if (p.d <= 64)
+        return p.dtype == 0 ? launch_generic_t<F32, 64>(p, stream)
+                            : launch_generic_t<BF16, 64>(p, stream);
+    return p.dtype == 0 ? launch_generic_t<F32, 128>(p, stream)
+                        : launch_generic_t<BF16, 128>(p, stream);
 }
 
 hipError_t launch_landmark_pool(const Problem &p, float *qbar, float *kbar, int32_t *map,

@@ -86,7 +86,7 @@ def fwd(L, q=P, k=P + (1 << 24), v=P + (2 << 24), o=P + (3 << 24), W=2, H=3, N=6
 def test_forward_validation(L):
     assert fwd(L, dtype=2) == EDTYPE
     assert fwd(L, dtype=-1) == EDTYPE
-    for kw in [dict(N=0), dict(N=(1 << 20) + 1), dict(d=0), dict(d=65), dict(m=0), dict(m=65, N=4096),
+    for kw in [dict(N=0), dict(N=(1 << 20) + 1), dict(d=0), dict(d=129), dict(m=0), dict(m=65, N=4096),
                dict(m=65), dict(W=-1), dict(H=-2), dict(N=63, m=7), dict(N=64, m=3),
                dict(W=1 << 16, H=1 << 16), dict(W=1 << 24, H=1), dict(W=1 << 23, H=2),
                dict(W=(1 << 23) + 1, H=2)]:
@@ -126,7 +126,7 @@ def test_exact_validation(L):
     q, k, v, o = P, P + (1 << 24), P + (2 << 24), P + (3 << 24)
     assert f(q, k, v, o, 2, 3, 64, 30, 7, 0.0, None) == EDTYPE
     assert f(q, k, v, o, 2, 3, 0, 30, 0, 0.0, None) == ESHAPE
-    assert f(q, k, v, o, 2, 3, 64, 65, 0, 0.0, None) == ESHAPE
+    assert f(q, k, v, o, 2, 3, 64, 129, 0, 0.0, None) == ESHAPE
     assert f(q, k, v, o, 2, 3, 64, 30, 0, float("nan"), None) == EARG
     assert f(None, k, v, o, 2, 3, 64, 30, 0, 0.0, None) == ENULL
     assert f(q, k, v, q + 8, 2, 3, 64, 30, 0, 0.0, None) == EOVERLAP
@@ -160,7 +160,7 @@ def test_status_strings_and_opts(L):
 
 def test_variant_selection():
     # tiled head widths: multiples of 4 from 8 to 32, and 30
-    for d in range(1, 65):
+    for d in range(1, 129):
         tiled = 8 <= d <= 32 and (d % 4 == 0 or d == 30)
         sel = B.nystra_select_variant(256, d, 16)
         assert sel == (B.VARIANT_TILED if tiled else B.VARIANT_GENERIC), d
@@ -257,7 +257,7 @@ def test_noalloc_rejects_more_than_its_scratch(L):
     assert b"NYSTRA_STATIC_SCRATCH_BYTES" in L.nystra_last_error()
     # the other validation paths are those of nystra_attn_forward_ws
     assert f(None, k, v, o, 1, 6, N_, d_, m_, 0, ctypes.byref(opts), None) == ENULL
-    assert f(q, k, v, o, 1, 6, N_, 65, m_, 0, ctypes.byref(opts), None) == ESHAPE
+    assert f(q, k, v, o, 1, 6, N_, 129, m_, 0, ctypes.byref(opts), None) == ESHAPE
     assert f(q, k, v, o, 0, 6, N_, d_, m_, 0, None, None) == OK
 
 

@@ -94,6 +94,10 @@ EDGE = [
     (1, 2, 1024, 16, 64, 1),  # 1-D segments at N = 1024
     (3, 2, 256, 8, 32, 1),    # 1-D segments, narrow head
     (2, 2, 240, 24, 48, 1),   # three landmark tiles, 1-D segments
+    (2, 1, 49, 65, 7, 0),     # first width past 64 (odd)
+    (2, 2, 64, 96, 16, 0),    # wide head at a config window
+    (1, 2, 256, 128, 64, 0),  # widest head with the most landmarks (largest LDS)
+    (1, 1, 1024, 128, 32, 1), # widest head, 1-D segments, long window
 ]
 
 
@@ -164,7 +168,8 @@ def test_landmark_pool(N, d, m, mode, dtype):
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("shape", [(4, 6, 64, 30), (16, 1, 64, 32), (2, 3, 256, 30),
                                    (1, 4, 1024, 32), (3, 2, 36, 7), (2, 1, 1, 1),
-                                   (1, 2, 4096, 8), (2, 2, 64, 64)])
+                                   (1, 2, 4096, 8), (2, 2, 64, 64), (2, 1, 49, 65),
+                                   (1, 2, 300, 128)])
 def test_exact_kernel(shape, dtype):
     q, k, v = W.iid(shape, seed=sum(shape), dtype=dtype)
     ref = oracle.exact(q, k, v)
