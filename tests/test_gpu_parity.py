@@ -94,6 +94,7 @@ EDGE = [
     (1, 2, 1024, 16, 64, 1),  # 1-D segments at N = 1024
     (3, 2, 256, 8, 32, 1),    # 1-D segments, narrow head
     (2, 2, 240, 24, 48, 1),   # three landmark tiles, 1-D segments
+    (2, 2, 384, 30, 24, 1),   # two landmark tiles, the second partly padding
     (2, 1, 49, 65, 7, 0),     # first width past 64 (odd)
     (2, 2, 64, 96, 16, 0),    # wide head at a config window
     (1, 2, 256, 128, 64, 0),  # widest head with the most landmarks (largest LDS)
@@ -129,14 +130,15 @@ def test_iteration_counts(iters, variant):
 
 
 @pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("iters", [0, 1, 5, 8])
-def test_iteration_counts_large_window(iters, variant):
+def test_iteration_counts_large_window(iters, dtype, variant):
     wl = W.CONFIGS["c4"]
-    need_variant(wl.N, wl.d, wl.m, "f32", variant)
-    q, k, v = W.generate(wl, "f32", n_windows=4)
+    need_variant(wl.N, wl.d, wl.m, dtype, variant)
+    q, k, v = W.generate(wl, dtype, n_windows=4)
     ref = oracle.forward(q, k, v, wl.m, iters=iters)
-    got = run(q, k, v, wl.m, "f32", variant, iters=iters)
-    check(got, ref, "f32", f"c4 K={iters} variant={variant}")
+    got = run(q, k, v, wl.m, dtype, variant, iters=iters)
+    check(got, ref, dtype, f"c4 K={iters} {dtype} variant={variant}")
 
 
 @pytest.mark.parametrize("variant", VARIANTS)
