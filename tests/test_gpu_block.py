@@ -60,6 +60,8 @@ CASES = [
     (1, 16, 16, 180, 6, 16, 8, 0, "bf16", "exact"),
     (1, 64, 64, 64, 2, 64, 0, 64, "f32", "nystrom"),    # one window per map: token-split path
     (1, 64, 64, 64, 2, 64, 32, 16, "bf16", "nystrom"),
+    (1, 16, 16, 256, 2, 8, 4, 16, "f32", "nystrom"),    # d_h = 128 (widest head)
+    (1, 16, 24, 192, 2, 8, 0, 8, "bf16", "nystrom"),    # d_h = 96
 ]
 
 
