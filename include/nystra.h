@@ -31,9 +31,11 @@
  *   bf16 for the P V product, as bf16 flash attention does (row sums fp32).
  * Streams.  `stream` is a hipStream_t (NULL = the null stream).  Work is
  *   enqueued and the call returns at once; the library never synchronises,
- *   allocates no device memory and keeps no mutable global state, so calls
- *   on different streams may overlap.  Faults inside a kernel surface at the
- *   caller's next synchronisation.
+ *   allocates no device memory and keeps no mutable global state (apart from
+ *   the static scratch of nystra_attn_forward_noalloc), so calls on
+ *   different streams may overlap.  Only kernel launches are enqueued (no
+ *   memory fills or copies), so a call can be recorded in a HIP graph.
+ *   Faults inside a kernel surface at the caller's next synchronisation.
  * Errors.  Every function returns an int status (nystra_status).  All
  *   argument checks run before anything is enqueued, so on any error other
  *   than NYSTRA_ERR_HIP no output is written.  n_windows == 0 or heads == 0
