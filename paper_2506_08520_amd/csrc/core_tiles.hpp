@@ -343,16 +343,22 @@ __device__ inline void landmark_core(float *lds, const float (&qb)[8], float mu,
             XLT[j] = read_lt<P>(Yb, lt, j, g, c);
 #pragma unroll
         for (int j = 0; j < MT; ++j)
-            write_tile<P>(Ya, lt, j, (j == lt ? eye * 7.f : zero4) - X[j], g, c);
+            write_tile<P>(Ya, lt, j, X[j], g, c);
         __syncthreads();
+        // The update in expanded form, the constants riding in the products'
+        // accumulators: Y1 = 15I - 7X + X X, N = X Y1 - 13I (= -Y2) and
+        // Z <- -(Z N) / 4.
         f4 Y[MT];
 #pragma unroll
         for (int j = 0; j < MT; ++j) {
-            f4 acc = zero4;
+            f4 acc;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                acc[i] = fmaf(X[j][i], -7.f, j == lt ? 15.f * eye[i] : 0.f);
 #pragma unroll
             for (int kk = 0; kk < MT; ++kk)
                 acc = mm16_acc(XLT[kk], read_r<P>(Ya, kk, j, g, c), acc);
-            Y[j] = (j == lt ? eye * 15.f : zero4) - acc;
+            Y[j] = acc;
         }
 #pragma unroll
         for (int j = 0; j < MT; ++j)
@@ -360,11 +366,11 @@ __device__ inline void landmark_core(float *lds, const float (&qb)[8], float mu,
         __syncthreads();
 #pragma unroll
         for (int j = 0; j < MT; ++j) {
-            f4 acc = zero4;
+            f4 acc = j == lt ? eye * -13.f : zero4;
 #pragma unroll
             for (int kk = 0; kk < MT; ++kk)
                 acc = mm16_acc(XLT[kk], read_r<P>(Yb, kk, j, g, c), acc);
-            Y[j] = (j == lt ? eye * 13.f : zero4) - acc;
+            Y[j] = acc;
         }
 #pragma unroll
         for (int j = 0; j < MT; ++j)
@@ -377,7 +383,7 @@ __device__ inline void landmark_core(float *lds, const float (&qb)[8], float mu,
 #pragma unroll
             for (int kk = 0; kk < MT; ++kk)
                 acc = mm16_acc(ZLT[kk], read_r<P>(Ya, kk, j, g, c), acc);
-            Zn[j] = acc * 0.25f;
+            Zn[j] = acc * -0.25f;
         }
 #pragma unroll
         for (int j = 0; j < MT; ++j)

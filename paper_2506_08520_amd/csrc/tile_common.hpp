@@ -150,10 +150,10 @@ __device__ inline SplitPair both_orders(bf8 hl)
 // the bf16 matrix cores with fp32 accumulation.  Pairing [hi | lo] with
 // [hi | lo] gives L_hi R_hi + L_lo R_lo; pairing [lo | hi] with [hi | lo]
 // gives the two cross terms; together the full product of the two sums.
-// mm16_hl takes LT = L^T in both orders, mm16_lh R in both orders.
-__device__ inline f4 mm16_hl(const SplitPair &LT, bf8 R)
+// mm16_hl takes LT = L^T in both orders (and adds acc), mm16_lh R in both orders.
+__device__ inline f4 mm16_hl(const SplitPair &LT, bf8 R, f4 acc = f4{0.f, 0.f, 0.f, 0.f})
 {
-    const f4 acc = mfma_bf16(LT.hl, R, f4{0.f, 0.f, 0.f, 0.f});
+    acc = mfma_bf16(LT.hl, R, acc);
     return mfma_bf16(LT.lh, R, acc);
 }
 

@@ -470,8 +470,9 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     // The factor 1/4 of the update rides on A: with X' = (A/4) Z = X/4,
     //   4 Y1 = 28I - 16X',  Y2 = 15I - X' (4 Y1),  Y3 / 4 = 13I/4 - X' Y2,
     // and Z <- Z (Y3 / 4).  Scaling by powers of two is exact, so every value
-    // equals the one of the update as written.
-    const f4 ATq = AT * 0.25f, e28 = eye * 28.f, e15 = eye * 15.f, e13q = eye * 3.25f;
+    // equals the one of the update as written.  The constants ride in the
+    // products' accumulators: -Y2 = X' (4 Y1) - 15I, Y3 / 4 = 13I/4 + X' (-Y2).
+    const f4 ATq = AT * 0.25f, e28 = eye * 28.f, en15 = eye * -15.f, e13q = eye * 3.25f;
     if constexpr (BFM) {
         // bf16 inputs: every product as (hi + lo) x (hi + lo) bf16 terms; the
         // left factors come in both k orders, X'^T and Z^T by moving the split
@@ -489,8 +490,8 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             f4 Y;
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                Y[i] = fmaf(X2[i], 16.f, fmaf(Xq[i], -28.f, e15[i]));
-            Y = e13q - mm16_hl(XTq, split_tile(Y).hl);
+                Y[i] = fmaf(X2[i], -16.f, fmaf(Xq[i], 28.f, en15[i]));   // -Y2
+            Y = mm16_hl(XTq, split_tile(Y).hl, e13q);   // 13I/4 - X' Y2
             Z = mm16_hl(ZTs, split_tile(Y).hl);
         };
         if constexpr (KF > 0) {
@@ -511,8 +512,8 @@ tiled_small_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 #pragma unroll
             for (int i = 0; i < 4; ++i)
                 Y[i] = fmaf(Xq[i], -16.f, e28[i]);
-            Y = e15 - mm16(XTq, Y);
-            Y = e13q - mm16(XTq, Y);
+            Y = mm16_acc(XTq, Y, en15);   // X' (4 Y1) - 15I = -Y2
+            Y = mm16_acc(XTq, Y, e13q);   // 13I/4 - X' Y2
             Z = mm16(ZT, Y);
             ZT = transpose16(Z, scr, g, c);
         };
@@ -833,7 +834,7 @@ tiled_small_mw_kernel(const typename E::T *__restrict__ q, const typename E::T *
 #pragma unroll
         for (int i = 0; i < 4; ++i)
             eye[i] = (4 * g + i == c && c < m) ? 1.f : 0.f;
-        const f4 ATq = AT * 0.25f, e28 = eye * 28.f, e15 = eye * 15.f, e13q = eye * 3.25f;
+        const f4 ATq = AT * 0.25f, e28 = eye * 28.f, en15 = eye * -15.f, e13q = eye * 3.25f;
         if constexpr (BFM) {
             const SplitPair Aq = both_orders(split_tile(ATq).hl);
             auto step = [&]() {
@@ -846,8 +847,8 @@ tiled_small_mw_kernel(const typename E::T *__restrict__ q, const typename E::T *
                 f4 Y;
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    Y[i] = fmaf(X2[i], 16.f, fmaf(Xq[i], -28.f, e15[i]));
-                Y = e13q - mm16_hl(XTq, split_tile(Y).hl);
+                    Y[i] = fmaf(X2[i], -16.f, fmaf(Xq[i], 28.f, en15[i]));   // -Y2
+                Y = mm16_hl(XTq, split_tile(Y).hl, e13q);   // 13I/4 - X' Y2
                 Z = mm16_hl(ZTs, split_tile(Y).hl);
             };
             if constexpr (KF > 0) {
@@ -868,8 +869,8 @@ tiled_small_mw_kernel(const typename E::T *__restrict__ q, const typename E::T *
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
                     Y[i] = fmaf(Xq[i], -16.f, e28[i]);
-                Y = e15 - mm16(XTq, Y);
-                Y = e13q - mm16(XTq, Y);
+                Y = mm16_acc(XTq, Y, en15);   // X' (4 Y1) - 15I = -Y2
+                Y = mm16_acc(XTq, Y, e13q);   // 13I/4 - X' Y2
                 Z = mm16(ZT, Y);
                 ZT = transpose16(Z, scr, g, c);
             };
