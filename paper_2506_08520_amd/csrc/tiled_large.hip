@@ -10,7 +10,10 @@
 //      landmark tile: running maxima of S_U over its keys, and G_U^n and
 //      T = G_U^n [V | 1] accumulated against them (rescaled whenever a maximum
 //      grows).  The waves' records are merged in LDS against the row maxima
-//      m_U over all keys.  Every K and V row is read once per unit.
+//      m_U over all keys.  Every K and V row is read once per unit.  With the
+//      patch grids of 16 x 16 and 32 x 32 windows (patches four tokens wide)
+//      and bf16 inputs, Step 1 for K happens here too (KP): each wave takes
+//      whole bands of patches and sums their K rows as they pass.
 //   3. Step 2 and Step 4: the wave builds its row tile of A = G_A^n; the m x m
 //      pseudo-inverse iteration runs with each wave computing its row tile of
 //      every product, the right-hand operands exchanged through LDS.
@@ -39,13 +42,15 @@ struct LargeArgs {
 };
 
 // FULL: m = 16 MT, so every landmark slot is real and the masks fold away.
-template <class E, int MT, int D, bool BFM, bool FULL>
+// KP: Kbar is pooled in the key pass (bf16, FULL, the grids kpool_ok accepts).
+template <class E, int MT, int D, bool BFM, bool FULL, bool KP>
 __global__ void __launch_bounds__(64 * MT)
 tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__restrict__ k,
                    const typename E::T *__restrict__ v, typename E::T *__restrict__ o,
                    LargeArgs a)
 {
     using L = LargeLds<MT>;
+    static_assert(!KP || (BFM && FULL), "K pooling in the key pass: bf16, full landmark tiles");
     constexpr int d = D;
     // With a spare column (D % 16 != 0), column D of V is replaced by ones, so
     // that column D of T, W and O carries T_D, W_D and O_D (no separate sums).
@@ -90,7 +95,8 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                     load_row8<D>(ku + t, y[u]);
                 } else {
                     xb[u] = *reinterpret_cast<const U16B *>(qu + t);
-                    yb[u] = *reinterpret_cast<const U16B *>(ku + t);
+                    if constexpr (!KP)
+                        yb[u] = *reinterpret_cast<const U16B *>(ku + t);
                 }
             }
 #pragma unroll
@@ -107,8 +113,10 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                         for (int w = 0; w < 4; ++w) {
                             qb[2 * w] += __uint_as_float(xb[u].w[w] << 16);
                             qb[2 * w + 1] += __uint_as_float(xb[u].w[w] & 0xffff0000u);
-                            kbv[2 * w] += __uint_as_float(yb[u].w[w] << 16);
-                            kbv[2 * w + 1] += __uint_as_float(yb[u].w[w] & 0xffff0000u);
+                            if constexpr (!KP) {
+                                kbv[2 * w] += __uint_as_float(yb[u].w[w] << 16);
+                                kbv[2 * w + 1] += __uint_as_float(yb[u].w[w] & 0xffff0000u);
+                            }
                         }
                     }
                 }
@@ -120,10 +128,12 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             kbv[s] = slot_valid<D>(g, s) ? kbv[s] * sc : 0.f;
         }
     }
+    if constexpr (!KP) {
 #pragma unroll
-    for (int s = 0; s < 8; ++s)
-        if (slot_valid<D>(g, s))
-            kbar[l * kTS + chunk_start<D>(g) + s] = kbv[s];
+        for (int s = 0; s < 8; ++s)
+            if (slot_valid<D>(g, s))
+                kbar[l * kTS + chunk_start<D>(g) + s] = kbv[s];
+    }
 
     // Qbar rows go to a table too, so that every wave can read every tile.
     float *qtab = lds + L::qtab;
@@ -131,7 +141,7 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     for (int s = 0; s < 8; ++s)
         if (slot_valid<D>(g, s))
             qtab[l * kTS + chunk_start<D>(g) + s] = qb[s];
-    __syncthreads();   // Qbar and Kbar complete
+    __syncthreads();   // Qbar (and, unless KP, Kbar) complete
 
     // ---- Step 3, G_U side.  The waves split the keys: wave lt takes the key
     // tile pairs 2lt, 2lt + 2MT, ... and, for every landmark tile j, keeps the
@@ -164,6 +174,39 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             TJ[j][ct] = f4{0.f, 0.f, 0.f, 0.f};
         tdj[j] = 0.f;
         mrj[j] = -INFINITY;
+    }
+    // The wave's key tile pairs: t0 = t_begin, t_begin + t_stride, ... below
+    // t_end.  Round-robin over the waves, or (KP) a contiguous block of whole
+    // patch bands: ppb pairs of tiles cover the rows of one band of patches.
+    int t_begin = 2 * lt, t_stride = 2 * MT, t_end = NT, ppb = 1;
+    if constexpr (KP) {
+        const int ppw = (NT >> 1) / MT;
+        t_begin = 2 * ppw * lt;
+        t_stride = 2;
+        t_end = t_begin + 2 * ppw;
+        ppb = (a.pr * (a.cols >> 4)) >> 1;
+    }
+    // KP: one-hot selectors that move feature 16ct + c of a K row into column
+    // c of a product (the valid slot holding it gets 1, every other slot 0),
+    // and per-lane partial patch sums pk[u][ct] of the band in progress.  A
+    // feature's valid slot lies in lane group f / 8, so lane (g, c) has a 1
+    // only in the selector of feature tile g / 2: one selector (ksel_own) is
+    // kept, the other tile's is zero.
+    U16B ksel_own = {{0u, 0u, 0u, 0u}};
+    float pk[2][2] = {{0.f, 0.f}, {0.f, 0.f}};
+    if constexpr (KP) {
+        const int f = 16 * (g >> 1) + c;
+#pragma unroll
+        for (int pp = 0; pp < 4; ++pp) {
+            uint32_t x = 0;
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int sl = 2 * pp + h;
+                if (slot_valid<D>(g, sl) && chunk_start<D>(g) + sl == f)
+                    x |= 0x3F80u << (16 * h);   // bf16 1.0
+            }
+            ksel_own.w[pp] = x;
+        }
     }
     // Pairs are software-pipelined: the next pair's K and V rows are requested
     // before this pair is computed (past the end they repeat the last tile,
@@ -319,23 +362,66 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                 }
             }
         }
+        if constexpr (KP) {
+            // Step 1 for K.  The product K_tile x ksel (tile ct) puts K[token
+            // 16tt + 4g + i][feature 16ct + c] in lane (g, c); the tokens 4g..4g+3
+            // of a tile are four adjacent columns of one image row, i.e. one
+            // patch row.  One tile per row (16 x 16 windows): both tiles of the
+            // pair are rows of the same patches, accumulated in one product.
+            // Two tiles per row (32 x 32): tile u holds columns 16u.., patches
+            // 4u + g.
+            const bool one_row_tile = a.cols == 16;   // uniform
+            const f4 z4 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ct = 0; ct < 2; ++ct) {
+                U16B sw;
+#pragma unroll
+                for (int pp = 0; pp < 4; ++pp)
+                    sw.w[pp] = (g >> 1) == ct ? ksel_own.w[pp] : 0u;
+                const bf8 ksel = __builtin_bit_cast(bf8, sw);
+                f4 d0 = mfma_bf16(kw_[0], ksel, z4);
+                if (one_row_tile) {
+                    d0 = mfma_bf16(kw_[1], ksel, d0);
+                } else {
+                    const f4 d1 = mfma_bf16(kw_[1], ksel, z4);
+                    pk[1][ct] += (d1[0] + d1[1]) + (d1[2] + d1[3]);
+                }
+                pk[0][ct] += (d0[0] + d0[1]) + (d0[2] + d0[3]);
+            }
+            const int pair = t0 >> 1;
+            if ((pair + 1) % ppb == 0) {   // uniform: the band is complete
+                const int band = pair / ppb;
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    if (u == 1 && one_row_tile)
+                        break;
+                    const int lk = band * a.gc + 4 * u + g;
+#pragma unroll
+                    for (int ct = 0; ct < 2; ++ct) {
+                        if (16 * ct + c < D)
+                            kbar[lk * kTS + 16 * ct + c] = pk[u][ct] * a.inv_patch;
+                        pk[u][ct] = 0.f;
+                    }
+                }
+            }
+        }
     };
     // Unrolled by two with two buffers (no loaded row is copied) where the
     // registers allow it; bf16 with three or four landmark tiles copies the
     // prefetched pair instead.
-    load_pair(2 * lt, kr, kw, vr, vh);
+    load_pair(t_begin, kr, kw, vr, vh);
     if constexpr (!(BFM && MT >= 3)) {
-        for (int t0 = 2 * lt; t0 < NT; t0 += 4 * MT) {
-            load_pair(t0 + 2 * MT, krn, kwn, vrn, vhn);
+        for (int t0 = t_begin; t0 < t_end; t0 += 2 * t_stride) {
+            load_pair(t0 + t_stride, krn, kwn, vrn, vhn);
             process(t0, kr, kw, vr, vh);
-            if (t0 + 2 * MT >= NT)
+            if (t0 + t_stride >= t_end)
                 break;   // uniform
-            load_pair(t0 + 4 * MT, kr, kw, vr, vh);
-            process(t0 + 2 * MT, krn, kwn, vrn, vhn);
+            load_pair(t0 + 2 * t_stride, kr, kw, vr, vh);
+            process(t0 + t_stride, krn, kwn, vrn, vhn);
         }
     } else {
-        for (int t0 = 2 * lt; t0 < NT; t0 += 2 * MT) {
-            load_pair(t0 + 2 * MT, krn, kwn, vrn, vhn);
+        for (int t0 = t_begin; t0 < t_end; t0 += t_stride) {
+            load_pair(t0 + t_stride, krn, kwn, vrn, vhn);
             process(t0, kr, kw, vr, vh);
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
@@ -407,7 +493,20 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     }
     const float mu = a.s2 * mrun;   // m_U of landmark l (base-2 units)
 
-    landmark_core<MT, D, BFM, FULL>(lds, qb, mu, T, tden, m, a.iters, a.s2, lt, lane);
+    // This lane's Qbar row, read back from its table (intact until the core
+    // overwrites the region, after its first barrier) rather than held in
+    // registers through the key pass: fewer registers for the fp32 and KP
+    // kernels (c4 fp32 -0.8%); the bf16 kernel without KP keeps its registers
+    // (+0.4% with the reload).
+    float qbl[8];
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+        if constexpr (KP || !BFM)
+            qbl[s] = slot_valid<D>(g, s) ? qtab[l * kTS + chunk_start<D>(g) + s] : 0.f;
+        else
+            qbl[s] = qb[s];
+    }
+    landmark_core<MT, D, BFM, FULL>(lds, qbl, mu, T, tden, m, a.iters, a.s2, lt, lane);
     constexpr int TDo = table_den<MT>();
     float *Wb = lds + L::wb;
 
@@ -584,6 +683,22 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 }
 
 // bf16 inputs with N % 32 == 0 take the bf16 matrix-core path.
+// K pooled in the key pass: square windows one or two 16-token tiles wide,
+// patches four tokens wide (a patch row is one lane group's four tokens of a
+// tile), whole bands of patches per wave.  Launched for four landmark tiles
+// only: with two (16 x 16 windows, m = 32) the kernel needs 138 VGPRs instead
+// of 124, one unit fewer per SIMD, and measured no faster.
+bool kpool_ok(const Problem &p, int MT)
+{
+    const Geometry &g = p.geo;
+    if (g.rows * g.cols != p.N || g.pc != 4 || (g.cols != 16 && g.cols != 32))
+        return false;
+    const int tpr = g.cols / 16, pairs = p.N / 32;
+    if ((g.pr * tpr) % 2 != 0 || pairs % MT != 0)
+        return false;
+    return (pairs / MT) % (g.pr * tpr / 2) == 0;
+}
+
 template <class E, int MT, int D, bool FULL>
 void launch_large_f(const Problem &p, const LargeArgs &a, hipStream_t stream)
 {
@@ -593,12 +708,20 @@ void launch_large_f(const Problem &p, const LargeArgs &a, hipStream_t stream)
     const auto *v = static_cast<const typename E::T *>(p.v);
     auto *o = static_cast<typename E::T *>(p.o);
     const dim3 grid(unsigned(p.units)), block(64 * MT);
-    if (E::bytes == 2 && p.N % 32 == 0)
-        hipLaunchKernelGGL((tiled_large_kernel<E, MT, D, E::bytes == 2, FULL>), grid, block,
-                           lds, stream, q, k, v, o, a);
-    else
-        hipLaunchKernelGGL((tiled_large_kernel<E, MT, D, false, FULL>), grid, block, lds,
+    if (E::bytes == 2 && p.N % 32 == 0) {
+        if constexpr (E::bytes == 2 && FULL && MT == 4) {
+            if (kpool_ok(p, MT)) {
+                hipLaunchKernelGGL((tiled_large_kernel<E, MT, D, true, true, true>), grid, block,
+                                   lds, stream, q, k, v, o, a);
+                return;
+            }
+        }
+        hipLaunchKernelGGL((tiled_large_kernel<E, MT, D, E::bytes == 2, FULL, false>), grid,
+                           block, lds, stream, q, k, v, o, a);
+    } else {
+        hipLaunchKernelGGL((tiled_large_kernel<E, MT, D, false, FULL, false>), grid, block, lds,
                            stream, q, k, v, o, a);
+    }
 }
 
 template <class E, int MT, int D>

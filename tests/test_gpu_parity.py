@@ -99,6 +99,9 @@ EDGE = [
     (2, 2, 64, 96, 16, 0),    # wide head at a config window
     (1, 2, 256, 128, 64, 0),  # widest head with the most landmarks (largest LDS)
     (1, 1, 1024, 128, 32, 1), # widest head, 1-D segments, long window
+    (2, 1, 1024, 8, 64, 0),   # K pooled in the key pass (bf16): narrowest head
+    (1, 2, 1024, 20, 64, 0),  # ... with overlapping feature chunks
+    (1, 3, 1024, 24, 64, 0),  # ... and a spare column at d = 24
 ]
 
 
