@@ -691,7 +691,7 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 bool kpool_ok(const Problem &p, int MT)
 {
     const Geometry &g = p.geo;
-    if (g.rows * g.cols != p.N || g.pc != 4 || (g.cols != 16 && g.cols != 32))
+    if (g.rows != g.cols || g.rows * g.cols != p.N || g.pc != 4 || (g.cols != 16 && g.cols != 32))
         return false;
     const int tpr = g.cols / 16, pairs = p.N / 32;
     if ((g.pr * tpr) % 2 != 0 || pairs % MT != 0)
