@@ -505,9 +505,8 @@ def measure(wl, dtype, args, q, k, v, headline):
             "kernel": "torch.addcmul: reads Q, K, V and writes O once, the bytes of one step",
             "kernel_ms": ckern, "achieved_GBs": cg, "frac": cg / HBM_PEAK_GBS,
             "nystrom_over_ceiling": gbs / cg}
-    if headline:
-        r["traffic"] = measured_traffic(wl.name, dtype, B.nystra_select_variant(
-            wl.N, wl.d, wl.m, code))
+    r["traffic"] = measured_traffic(wl.name, dtype, B.nystra_select_variant(
+        wl.N, wl.d, wl.m, code))
     del case
     torch.cuda.empty_cache()
     return r

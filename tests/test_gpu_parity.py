@@ -145,6 +145,19 @@ def test_iteration_counts_large_window(iters, dtype, variant):
 
 
 @pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("iters", [0, 1, 5, 8])
+def test_iteration_counts_pooled_keys(iters, variant):
+    """32 x 32 windows with m = 64 in bf16: the kernel that pools K in its key
+    pass, over the iteration range."""
+    wl = W.CONFIGS["c5"]
+    need_variant(wl.N, wl.d, wl.m, "bf16", variant)
+    q, k, v = W.generate(wl, "bf16", n_windows=1)
+    ref = oracle.forward(q, k, v, wl.m, iters=iters)
+    got = run(q, k, v, wl.m, "bf16", variant, iters=iters)
+    check(got, ref, "bf16", f"c5 K={iters} variant={variant}")
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
 def test_custom_scale(variant):
     need_variant(64, 30, 16, "f32", variant)
     q, k, v = W.iid((4, 2, 64, 30), seed=77)
