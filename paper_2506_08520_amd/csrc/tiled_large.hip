@@ -42,14 +42,21 @@ struct LargeArgs {
 };
 
 // FULL: m = 16 MT, so every landmark slot is real and the masks fold away.
-// KP: Kbar is pooled in the key pass (bf16, FULL, the grids kpool_ok accepts).
-template <class E, int MT, int D, bool BFM, bool FULL, bool KP>
+// KPL: 0 = Kbar pooled before the key pass; otherwise pooled in it (bf16,
+// FULL, the grids kpool_ok accepts): 1 = one 16-token tile per image row and
+// one pair of tiles per band of patches (16 x 16 windows, 2 x 4 patches),
+// 2 = two tiles per image row (32 x 32 windows), any band height.  With KPL = 1 the registers
+// are held to 128 (four waves per SIMD, as without KP); the few values that
+// do not fit are saved once around the key pass, none inside it.
+template <class E, int MT, int D, bool BFM, bool FULL, int KPL>
 __global__ void __launch_bounds__(64 * MT)
+__attribute__((amdgpu_waves_per_eu(KPL == 1 ? 4 : 1)))
 tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__restrict__ k,
                    const typename E::T *__restrict__ v, typename E::T *__restrict__ o,
                    LargeArgs a)
 {
     using L = LargeLds<MT>;
+    constexpr bool KP = KPL != 0;
     static_assert(!KP || (BFM && FULL), "K pooling in the key pass: bf16, full landmark tiles");
     constexpr int d = D;
     // With a spare column (D % 16 != 0), column D of V is replaced by ones, so
@@ -184,17 +191,17 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
         t_begin = 2 * ppw * lt;
         t_stride = 2;
         t_end = t_begin + 2 * ppw;
-        ppb = (a.pr * (a.cols >> 4)) >> 1;
+        ppb = KPL == 1 ? 1 : (a.pr * (a.cols >> 4)) >> 1;
     }
     // KP: one-hot selectors that move feature 16ct + c of a K row into column
     // c of a product (the valid slot holding it gets 1, every other slot 0),
     // and per-lane partial patch sums pk[u][ct] of the band in progress.  A
     // feature's valid slot lies in lane group f / 8, so lane (g, c) has a 1
     // only in the selector of feature tile g / 2: one selector (ksel_own) is
-    // kept, the other tile's is zero.
-    U16B ksel_own = {{0u, 0u, 0u, 0u}};
-    float pk[2][2] = {{0.f, 0.f}, {0.f, 0.f}};
-    if constexpr (KP) {
+    // built, the other tile's is zero.  KPL = 1 rebuilds it per pair (fewer
+    // registers held through the loop).
+    auto own_selector = [&]() {
+        U16B w;
         const int f = 16 * (g >> 1) + c;
 #pragma unroll
         for (int pp = 0; pp < 4; ++pp) {
@@ -205,9 +212,14 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                 if (slot_valid<D>(g, sl) && chunk_start<D>(g) + sl == f)
                     x |= 0x3F80u << (16 * h);   // bf16 1.0
             }
-            ksel_own.w[pp] = x;
+            w.w[pp] = x;
         }
-    }
+        return w;
+    };
+    U16B ksel_own = {{0u, 0u, 0u, 0u}};
+    float pk[2][2] = {{0.f, 0.f}, {0.f, 0.f}};
+    if constexpr (KPL == 2)
+        ksel_own = own_selector();
     // Pairs are software-pipelined: the next pair's K and V rows are requested
     // before this pair is computed (past the end they repeat the last tile,
     // unused).  bf16 V is held as pairs of rows (4g, 4g+1) and (4g+2, 4g+3) of
@@ -370,7 +382,9 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
             // pair are rows of the same patches, accumulated in one product.
             // Two tiles per row (32 x 32): tile u holds columns 16u.., patches
             // 4u + g.
-            const bool one_row_tile = a.cols == 16;   // uniform
+            constexpr bool one_row_tile = KPL == 1;
+            if constexpr (KPL == 1)
+                ksel_own = own_selector();
             const f4 z4 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ct = 0; ct < 2; ++ct) {
@@ -380,7 +394,7 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                     sw.w[pp] = (g >> 1) == ct ? ksel_own.w[pp] : 0u;
                 const bf8 ksel = __builtin_bit_cast(bf8, sw);
                 f4 d0 = mfma_bf16(kw_[0], ksel, z4);
-                if (one_row_tile) {
+                if constexpr (one_row_tile) {
                     d0 = mfma_bf16(kw_[1], ksel, d0);
                 } else {
                     const f4 d1 = mfma_bf16(kw_[1], ksel, z4);
@@ -389,12 +403,12 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
                 pk[0][ct] += (d0[0] + d0[1]) + (d0[2] + d0[3]);
             }
             const int pair = t0 >> 1;
-            if ((pair + 1) % ppb == 0) {   // uniform: the band is complete
-                const int band = pair / ppb;
+            if (KPL == 1 || (pair + 1) % ppb == 0) {   // uniform: the band is complete
+                const int band = KPL == 1 ? pair : pair / ppb;
 #pragma unroll
                 for (int u = 0; u < 2; ++u) {
                     if (u == 1 && one_row_tile)
-                        break;
+                        break;   // compile-time
                     const int lk = band * a.gc + 4 * u + g;
 #pragma unroll
                     for (int ct = 0; ct < 2; ++ct) {
@@ -685,9 +699,7 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 // bf16 inputs with N % 32 == 0 take the bf16 matrix-core path.
 // K pooled in the key pass: square windows one or two 16-token tiles wide,
 // patches four tokens wide (a patch row is one lane group's four tokens of a
-// tile), whole bands of patches per wave.  Launched for four landmark tiles
-// only: with two (16 x 16 windows, m = 32) the kernel needs 138 VGPRs instead
-// of 124, one unit fewer per SIMD, and measured no faster.
+// tile), whole bands of patches per wave.
 bool kpool_ok(const Problem &p, int MT)
 {
     const Geometry &g = p.geo;
@@ -709,17 +721,27 @@ void launch_large_f(const Problem &p, const LargeArgs &a, hipStream_t stream)
     auto *o = static_cast<typename E::T *>(p.o);
     const dim3 grid(unsigned(p.units)), block(64 * MT);
     if (E::bytes == 2 && p.N % 32 == 0) {
-        if constexpr (E::bytes == 2 && FULL && MT == 4) {
-            if (kpool_ok(p, MT)) {
-                hipLaunchKernelGGL((tiled_large_kernel<E, MT, D, true, true, true>), grid, block,
+        // KP for two landmark tiles (16 x 16 windows, m = 32, 2 x 4 patches) and
+        // four (32 x 32, m = 64, 4 x 4 patches); other shapes keep the pooling
+        // loop.
+        if constexpr (E::bytes == 2 && FULL && MT == 2) {
+            if (kpool_ok(p, MT) && p.geo.cols == 16 && p.geo.pr == 2) {
+                hipLaunchKernelGGL((tiled_large_kernel<E, MT, D, true, true, 1>), grid, block,
                                    lds, stream, q, k, v, o, a);
                 return;
             }
         }
-        hipLaunchKernelGGL((tiled_large_kernel<E, MT, D, E::bytes == 2, FULL, false>), grid,
+        if constexpr (E::bytes == 2 && FULL && MT == 4) {
+            if (kpool_ok(p, MT) && p.geo.cols == 32) {
+                hipLaunchKernelGGL((tiled_large_kernel<E, MT, D, true, true, 2>), grid, block,
+                                   lds, stream, q, k, v, o, a);
+                return;
+            }
+        }
+        hipLaunchKernelGGL((tiled_large_kernel<E, MT, D, E::bytes == 2, FULL, 0>), grid,
                            block, lds, stream, q, k, v, o, a);
     } else {
-        hipLaunchKernelGGL((tiled_large_kernel<E, MT, D, false, FULL, false>), grid, block, lds,
+        hipLaunchKernelGGL((tiled_large_kernel<E, MT, D, false, FULL, 0>), grid, block, lds,
                            stream, q, k, v, o, a);
     }
 }

@@ -102,6 +102,8 @@ EDGE = [
     (2, 1, 1024, 8, 64, 0),   # K pooled in the key pass (bf16): narrowest head
     (1, 2, 1024, 20, 64, 0),  # ... with overlapping feature chunks
     (1, 3, 1024, 24, 64, 0),  # ... and a spare column at d = 24
+    (3, 2, 256, 8, 32, 0),    # ... 16 x 16 windows (one tile per image row)
+    (2, 2, 256, 20, 32, 0),   # ... 16 x 16, overlapping chunks
 ]
 
 
