@@ -83,9 +83,16 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
     for (int s = 0; s < 8; ++s)
         qb[s] = kbv[s] = 0.f;
     {
+        // KPL 2 fixes the grid (32 columns, 4 x 4 patches, 8 per row), so the
+        // token offsets below are shifts and masks (c5 -1.3%; the same for
+        // KPL 1 measured +0.9%); otherwise they come from a.
+        const int gcols = KPL == 2 ? 32 : a.cols;
+        const int gpr = KPL == 2 ? 4 : a.pr;
+        const int gpc = KPL == 2 ? 4 : a.pc;
+        const int ggc = KPL == 2 ? 8 : a.gc;
         const int le = lval ? l : m - 1;   // padding lanes read a valid patch, then drop it
-        const int r0 = (le / a.gc) * a.pr, c0 = (le % a.gc) * a.pc;
-        const int npatch = a.pr * a.pc;
+        const int r0 = (le / ggc) * gpr, c0 = (le % ggc) * gpc;
+        const int npatch = gpr * gpc;
         // Rows arrive raw; the slots a lower lane group carries are zeroed
         // once, in the sums (the same values as zeroing every row).
         constexpr int kP = 8;
@@ -95,7 +102,7 @@ tiled_large_kernel(const typename E::T *__restrict__ q, const typename E::T *__r
 #pragma unroll
             for (int u = 0; u < kP; ++u) {
                 const int j = min(j0 + u, npatch - 1);
-                const int64_t t = (int64_t(r0 + j / a.pc) * a.cols + c0 + j % a.pc) * d +
+                const int64_t t = (int64_t(r0 + j / gpc) * gcols + c0 + j % gpc) * d +
                                   chunk_start<D>(g);
                 if constexpr (E::bytes == 4) {
                     load_row8<D>(qu + t, x[u]);
