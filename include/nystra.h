@@ -208,8 +208,9 @@ int nystra_attn_forward_noalloc(const void *Q, const void *K, const void *V, voi
  * divides channels, d_h <= 128, channels <= 4096, batch * height * width
  * <= 2^31 - 1, and the attention limits above for N, m and the unit count.
  * nystra_block_workspace_size: host-only size of the workspace
- * nystra_block_forward needs (Q, K, V, O and, for long windows, the
- * token-split workspace).  nystra_block_forward: workspace as for
+ * nystra_block_forward needs (Q, K, V, O, for channels <= 256 the two weight
+ * matrices repacked into the GEMM's tile layout (written by each call), and
+ * for long windows the token-split workspace).  nystra_block_forward: workspace as for
  * nystra_attn_forward_ws (256-byte aligned, disjoint from every other
  * argument, NYSTRA_ERR_WORKSPACE otherwise); Y must not overlap X, the
  * weights or the biases. */

@@ -469,11 +469,13 @@ int nystra_select_variant(int N, int d_h, int m, int dtype, const nystra_opts *o
 
 namespace {
 
-// Workspace layout of the block: Q, K, V, O, then the attention's own.
+// Workspace layout of the block: Q, K, V, O, the packed weights of the two
+// GEMMs (when C <= 256), then the attention's own.
 struct BlockPlan {
     Problem p;          // the attention problem on the workspace tensors
     int variant;        // attention kernel family (Nystrom) or -1 (exact)
     size_t qkvo_bytes;  // one of the four tensors, padded to 256 bytes
+    size_t pk_qkv, pk_proj;   // packed W_qkv and W_proj, padded to 256 bytes (0: none)
     size_t bytes;       // total
 };
 
@@ -521,7 +523,9 @@ int plan_block(const nystra_block_shape *s, int m, int dtype, const nystra_opts 
     if (rc != NYSTRA_OK)
         return rc;
     bp->qkvo_bytes = pad256(size_t(rows) * s->channels * dtype_bytes(dtype));
-    bp->bytes = 4 * bp->qkvo_bytes;
+    bp->pk_qkv = pad256(nystra::block_wpack_bytes(s->channels, 3 * s->channels, dtype));
+    bp->pk_proj = pad256(nystra::block_wpack_bytes(s->channels, s->channels, dtype));
+    bp->bytes = 4 * bp->qkvo_bytes + bp->pk_qkv + bp->pk_proj;
     if (bp->variant == NYSTRA_VARIANT_SPLIT && bp->p.units > 0)
         bp->bytes += nystra::split_workspace_bytes(bp->p);
     return NYSTRA_OK;
@@ -577,7 +581,16 @@ int nystra_block_forward(const void *X, const void *Wqkv, const void *bqkv, cons
     char *ws = static_cast<char *>(workspace);
     void *q = ws, *k = ws + bp.qkvo_bytes, *v = ws + 2 * bp.qkvo_bytes,
          *o = ws + 3 * bp.qkvo_bytes;
+    char *pkq = bp.pk_qkv ? ws + 4 * bp.qkvo_bytes : nullptr;
+    char *pkp = bp.pk_qkv ? pkq + bp.pk_qkv : nullptr;
+    char *attn_ws = ws + 4 * bp.qkvo_bytes + bp.pk_qkv + bp.pk_proj;
     hipStream_t st = static_cast<hipStream_t>(stream);
+    clear_stale_error();
+    if (pkq) {
+        const hipError_t e = nystra::launch_block_wpack(Wqkv, Wproj, C, dtype, pkq, pkp, st);
+        if (e != hipSuccess)
+            return finish_launch(e);
+    }
     nystra::BlockGemm g;
     g.rows = rows;
     g.H = shape->height;
@@ -590,11 +603,11 @@ int nystra_block_forward(const void *X, const void *Wqkv, const void *bqkv, cons
     g.proj = false;
     g.a = X;
     g.wt = Wqkv;
+    g.wpk = pkq;
     g.bias = bqkv;
     g.out0 = q;
     g.out1 = k;
     g.out2 = v;
-    clear_stale_error();
     hipError_t e = nystra::launch_block_gemm(g, st);
     if (e != hipSuccess)
         return finish_launch(e);
@@ -606,7 +619,7 @@ int nystra_block_forward(const void *X, const void *Wqkv, const void *bqkv, cons
     if (bp.variant == -1)
         e = nystra::launch_exact(p, st);
     else if (bp.variant == NYSTRA_VARIANT_SPLIT)
-        e = nystra::launch_split(p, ws + 4 * bp.qkvo_bytes, st);
+        e = nystra::launch_split(p, attn_ws, st);
     else if (bp.variant == NYSTRA_VARIANT_TILED && nystra::tiled_supported(p))
         e = nystra::launch_tiled_forward(p, st);
     else
@@ -616,6 +629,7 @@ int nystra_block_forward(const void *X, const void *Wqkv, const void *bqkv, cons
     g.proj = true;
     g.a = o;
     g.wt = Wproj;
+    g.wpk = pkp;
     g.bias = bproj;
     g.out0 = Y;
     g.out1 = g.out2 = nullptr;

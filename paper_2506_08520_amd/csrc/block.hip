@@ -31,6 +31,7 @@ struct BlockArgs {
     int rtiles, ctiles;           // tile grid
     const void *a;                // X (QKV) or O (PROJ)
     const void *wt;               // [C][ncols]
+    const void *wpk;              // wt packed as the register-resident kernel's LDS tiles
     const void *bias;             // [ncols] or null
     void *out0, *out1, *out2;     // Q, K, V (QKV) or Y (PROJ)
 };
@@ -249,6 +250,49 @@ struct RkLds {
     static constexpr int total = 2 * tile > astage ? 2 * tile : astage;
 };
 
+// Packs W [C][ncols] into the LDS images of its 64-column tiles, one tile
+// after another: bf16 [n][k] with pitch PH (element (k, n0 + n) at n PH + k),
+// fp32 [k][PF] with the four 16-column tiles' values of column c at 4c + t
+// (element (k, n0 + 16t + c)).  Every slot outside W (k >= C, n >= ncols, the
+// pitch padding) is zero.  One thread per 4-byte word; the second matrix's
+// words follow the first's in the grid.
+struct WPackArgs {
+    const void *w0, *w1;   // W_qkv [C][3C], W_proj [C][C]
+    uint32_t *d0, *d1;     // their packed images
+    int C, words0, words1;
+};
+
+template <class E, int KP>
+__global__ void __launch_bounds__(256) block_wpack_kernel(WPackArgs p)
+{
+    using L = RkLds<E, KP>;
+    const int64_t gi = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    const bool second = gi >= p.words0;
+    const int64_t wi = second ? gi - p.words0 : gi;
+    if (wi >= (second ? p.words1 : p.words0))
+        return;
+    const int ncols = second ? p.C : 3 * p.C;
+    const typename E::T *W = static_cast<const typename E::T *>(second ? p.w1 : p.w0);
+    const int ct = int(wi / L::tile), w = int(wi - int64_t(ct) * L::tile), n0 = 64 * ct;
+    auto elem = [&](int k, int n) -> uint32_t {
+        if (k >= p.C || n >= ncols)
+            return 0u;
+        if constexpr (E::bytes == 2)
+            return uint32_t(reinterpret_cast<const uint16_t *>(W)[int64_t(k) * ncols + n]);
+        else
+            return __float_as_uint(W[int64_t(k) * ncols + n]);
+    };
+    uint32_t out;
+    if constexpr (E::bytes == 2) {
+        const int h = 2 * w, n = h / L::PH, k = h - n * L::PH;   // PH even: one row
+        out = k < KP ? elem(k, n0 + n) | (elem(k + 1, n0 + n) << 16) : 0u;
+    } else {
+        const int k = w / L::PF, r = w - k * L::PF;
+        out = r < 64 ? elem(k, n0 + 16 * (r & 3) + (r >> 2)) : 0u;
+    }
+    (second ? p.d1 : p.d0)[wi] = out;
+}
+
 template <class E, bool PROJ, int KP>
 __global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs a)
 {
@@ -323,71 +367,43 @@ __global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs 
     }
     __syncthreads();   // the stage becomes the W tiles
 
-    // ---- W tiles: global -> registers -> LDS.  A thread gathers one column's
-    // values for several k (lanes take consecutive columns, so every load is
-    // coalesced) and writes them with one 16-byte LDS store: bf16 eight k of
-    // column n into [n][k]; fp32 the four 16-column tiles' values of column
-    // c at one k into [k][c][t].
-    constexpr int kPieces = BF ? KP * 8 : KP * 16;   // 16-byte LDS pieces of a tile
+    // ---- W tiles: the packed image of each 64-column tile (block_wpack_kernel
+    // lays it out exactly as the LDS tile below, padding included) is copied
+    // global -> registers -> LDS in 16-byte pieces, consecutive lanes taking
+    // consecutive pieces: coalesced loads, conflict-free stores, no index
+    // arithmetic per element.
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    constexpr int kPieces = L::tile / 4;   // 16-byte pieces of a tile image
     constexpr int kPer = (kPieces + 64 * kRkWaves - 1) / (64 * kRkWaves);
-    U16B wr[kPer];
+    u32x4 wr[kPer];
     const int nct = (a.ncols + 63) / 64;
-    const typename E::T *W = static_cast<const typename E::T *>(a.wt);
-    // Every load reads an in-bounds address (k and n clamped) and the padding
-    // (k >= C, n >= ncols) is zeroed by a select, so the loop has no branches.
-    // Offsets are 32-bit (the host keeps every tensor under 2^31 elements).
+    const u32x4 *wsrc = static_cast<const u32x4 *>(a.wpk);
     auto wfetch = [&](int ct) {
-        const int n0 = 64 * ct;
+        const u32x4 *src = wsrc + int64_t(ct) * kPieces;
 #pragma unroll
-        for (int j = 0; j < kPer; ++j) {
+        for (int j = 0; j < kPer; ++j) {   // past the image: re-read its last piece
             const int idx = tid + j * 64 * kRkWaves;
-            U16B u = {{0u, 0u, 0u, 0u}};
-            if (kPer * 64 * kRkWaves == kPieces || idx < kPieces) {
-                if constexpr (BF) {
-                    const int n = n0 + (idx & 63), k0 = 8 * (idx >> 6);
-                    const bool nok = n < a.ncols;
-                    const int nc = nok ? n : a.ncols - 1;
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const int k = k0 + e;
-                        const bool ok = nok && k < a.C;
-                        const uint32_t h =
-                            uint32_t(W[(k < a.C ? k : a.C - 1) * a.ncols + nc]);
-                        u.w[e >> 1] |= (ok ? h : 0u) << (16 * (e & 1));
-                    }
-                } else {
-                    const int cc = idx & 15, k = idx >> 4;
-                    const int kc = k < a.C ? k : a.C - 1;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int n = n0 + 16 * e + cc;
-                        const bool ok = k < a.C && n < a.ncols;
-                        const float x = W[kc * a.ncols + (n < a.ncols ? n : a.ncols - 1)];
-                        u.w[e] = ok ? __float_as_uint(x) : 0u;
-                    }
-                }
-            }
-            wr[j] = u;
+            wr[j] = src[idx < kPieces ? idx : kPieces - 1];
         }
     };
     auto wstash = [&](int buf) {
-        float *dst = wbuf(buf);
+        u32x4 *dst = reinterpret_cast<u32x4 *>(wbuf(buf));
 #pragma unroll
         for (int j = 0; j < kPer; ++j) {
             const int idx = tid + j * 64 * kRkWaves;
-            if (kPer * 64 * kRkWaves > kPieces && idx >= kPieces)
-                break;
-            if constexpr (BF)
-                *reinterpret_cast<U16B *>(reinterpret_cast<uint16_t *>(dst) +
-                                          (idx & 63) * L::PH + 8 * (idx >> 6)) = wr[j];
-            else
-                *reinterpret_cast<U16B *>(dst + (idx >> 4) * L::PF + 4 * (idx & 15)) = wr[j];
+            if (kPer * 64 * kRkWaves == kPieces || idx < kPieces)
+                dst[idx] = wr[j];
         }
     };
     // Column part of the destination for the 64 columns of the current tile:
-    // which output tensor, and (QKV) head h, feature f -> h N d_h + f.
+    // which output tensor, and (QKV) head h, feature f -> h N d_h + f.  The
+    // bias of every column is staged in LDS once: a global load in the
+    // epilogue would wait behind the next tile's W pieces in flight.
     __shared__ int coltab[2][64];
     __shared__ int colwhich[2][64];
+    __shared__ float colbias[3 * 256];
+    for (int n = tid; n < a.ncols; n += 64 * kRkWaves)
+        colbias[n] = a.bias ? ld<E>(a.bias, n) : 0.f;
     auto cfill = [&](int ct, int buf) {
         if (tid < 64) {
             const int n = 64 * ct + tid;
@@ -403,19 +419,20 @@ __global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs 
         }
     };
 
-    // Row part of the destination of this lane's output rows 4g + i (-1: past
-    // the end): QKV (window wn, token tt) -> wn N C + tt d_h; PROJ -> pixel C.
-    int rowoff[4];
+    // Row part of the destination of this lane's output rows 4g + i: QKV
+    // (window wn, token tt) -> wn N C + tt d_h; PROJ -> pixel C.  Offsets are
+    // unsigned 32-bit (tensors under 2^31 elements); rows past the end are
+    // not stored.
+    uint32_t rowoff[4];
+    bool rowok[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int row = int(m0) + 16 * wv + 4 * g + i;   // rows < 2^31
-        if (row >= a.rows) {
-            rowoff[i] = -1;
-            continue;
-        }
-        const int wn = row / a.N, tt = row - wn * a.N;
-        rowoff[i] = int(PROJ ? pixel_of(a, wn, tt) * a.C
-                             : int64_t(wn) * a.N * a.C + int64_t(tt) * a.dh);
+        rowok[i] = row < a.rows;
+        const int rr = rowok[i] ? row : 0;
+        const int wn = rr / a.N, tt = rr - wn * a.N;
+        rowoff[i] = uint32_t(PROJ ? pixel_of(a, wn, tt) * a.C
+                                  : int64_t(wn) * a.N * a.C + int64_t(tt) * a.dh);
     }
 
     // Workgroups start at different column tiles, so that at any moment they
@@ -462,14 +479,14 @@ __global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs 
             const int n = 64 * ct + 16 * q + c;
             if (n >= a.ncols)
                 continue;
-            const float bias = a.bias ? ld<E>(a.bias, n) : 0.f;
-            const int col = coltab[it & 1][16 * q + c];
+            const float bias = colbias[n];
+            const uint32_t col = uint32_t(coltab[it & 1][16 * q + c]);
             const int which = colwhich[it & 1][16 * q + c];
             typename E::T *dst = static_cast<typename E::T *>(which == 0 ? a.out0
                                                               : which == 1 ? a.out1 : a.out2);
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                if (rowoff[i] >= 0) {
+                if (rowok[i]) {
                     const float v = acc[q][i] + bias;
                     if constexpr (BF)
                         dst[rowoff[i] + col] = uint16_t(cvt_bf16x2(v, 0.f));   // RNE
@@ -496,15 +513,13 @@ void launch_rk(const BlockArgs &a, hipStream_t stream)
 template <class E, bool PROJ>
 bool try_rk(const BlockArgs &a, hipStream_t stream)
 {
-    // 16-byte W pieces: fp32 rows 16-byte aligned, bf16 rows 4-byte aligned
+    if (!a.wpk)
+        return false;   // the weights were not packed (C > 256)
     if (a.rows * int64_t(a.C) >= (int64_t(1) << 31) ||
         int64_t(a.C) * a.ncols >= (int64_t(1) << 31))
         return false;   // 32-bit element offsets
     if ((a.rows + kRkRows - 1) / kRkRows * 64 * kRkWaves >= (int64_t(1) << 32))
         return false;   // fewer than 2^32 work-items in the grid
-    const uintptr_t wp = uintptr_t(a.wt);
-    if (E::bytes == 4 ? (wp % 16 != 0 || a.ncols % 4 != 0) : (wp % 4 != 0 || a.ncols % 2 != 0))
-        return false;
     // A as 4-byte words: bf16 needs an even C, and in PROJ an even d_h (a word
     // never straddles two heads); the A base 4-byte aligned
     if (uintptr_t(a.a) % 4 != 0 || (E::bytes == 2 && (a.C % 2 != 0 || (PROJ && a.dh % 2 != 0))))
@@ -541,6 +556,74 @@ bool block_gemm_supported(int64_t rows, int C)
     return rt * ct * 256 < (int64_t(1) << 32);
 }
 
+// Contraction length of the register-resident kernel for C (0: not used).
+static int rk_kp(int C)
+{
+    return C <= 32 ? 32 : C <= 64 ? 64 : C <= 128 ? 128 : C <= 192 ? 192 : C <= 256 ? 256 : 0;
+}
+
+template <class E, int KP>
+size_t wpack_words(int ncols)
+{
+    return size_t((ncols + 63) / 64) * RkLds<E, KP>::tile;
+}
+
+template <class E>
+size_t wpack_words_e(int C, int ncols)
+{
+    switch (rk_kp(C)) {
+    case 32: return wpack_words<E, 32>(ncols);
+    case 64: return wpack_words<E, 64>(ncols);
+    case 128: return wpack_words<E, 128>(ncols);
+    case 192: return wpack_words<E, 192>(ncols);
+    case 256: return wpack_words<E, 256>(ncols);
+    default: return 0;
+    }
+}
+
+size_t block_wpack_bytes(int C, int ncols, int dtype)
+{
+    return 4 * (dtype == 0 ? wpack_words_e<F32>(C, ncols) : wpack_words_e<BF16>(C, ncols));
+}
+
+template <class E, int KP>
+void launch_wpack_k(const WPackArgs &p, hipStream_t stream)
+{
+    const int64_t words = int64_t(p.words0) + p.words1;
+    hipLaunchKernelGGL((block_wpack_kernel<E, KP>), dim3(unsigned((words + 255) / 256)), dim3(256),
+                       0, stream, p);
+}
+
+template <class E>
+void launch_wpack_e(const WPackArgs &p, hipStream_t stream)
+{
+    switch (rk_kp(p.C)) {
+    case 32: launch_wpack_k<E, 32>(p, stream); break;
+    case 64: launch_wpack_k<E, 64>(p, stream); break;
+    case 128: launch_wpack_k<E, 128>(p, stream); break;
+    case 192: launch_wpack_k<E, 192>(p, stream); break;
+    default: launch_wpack_k<E, 256>(p, stream); break;
+    }
+}
+
+hipError_t launch_block_wpack(const void *wqkv, const void *wproj, int C, int dtype, void *pk_qkv,
+                              void *pk_proj, hipStream_t stream)
+{
+    WPackArgs p;
+    p.w0 = wqkv;
+    p.w1 = wproj;
+    p.d0 = static_cast<uint32_t *>(pk_qkv);
+    p.d1 = static_cast<uint32_t *>(pk_proj);
+    p.C = C;
+    p.words0 = int(block_wpack_bytes(C, 3 * C, dtype) / 4);
+    p.words1 = int(block_wpack_bytes(C, C, dtype) / 4);
+    if (dtype == 0)
+        launch_wpack_e<F32>(p, stream);
+    else
+        launch_wpack_e<BF16>(p, stream);
+    return hipGetLastError();
+}
+
 hipError_t launch_block_gemm(const BlockGemm &g, hipStream_t stream)
 {
     BlockArgs a;
@@ -560,6 +643,7 @@ hipError_t launch_block_gemm(const BlockGemm &g, hipStream_t stream)
     a.ctiles = (a.ncols + kBN - 1) / kBN;
     a.a = g.a;
     a.wt = g.wt;
+    a.wpk = g.wpk;
     a.bias = g.bias;
     a.out0 = g.out0;
     a.out1 = g.out1;

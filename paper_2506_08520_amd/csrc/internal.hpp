@@ -56,15 +56,22 @@ hipError_t launch_split(const Problem &p, void *workspace, hipStream_t stream);
 // are the pixels of X in window order, outputs go to Q, K, V (out0..2) in
 // [window][head][N][d_h].  PROJ: A rows gather the heads of O, outputs go to
 // the pixels of Y (out0).  Weights are [C][3C] or [C][C]; bias may be null.
+// wpk: the weights packed by launch_block_wpack (C <= 256), or null.
 struct BlockGemm {
     int64_t rows;     // B H W
     int H, W, C, heads, w, shift, dtype;
     bool proj;
-    const void *a, *wt, *bias;
+    const void *a, *wt, *bias, *wpk;
     void *out0, *out1, *out2;
 };
 bool block_gemm_supported(int64_t rows, int C);
 hipError_t launch_block_gemm(const BlockGemm &g, hipStream_t stream);
+// Bytes of the packed image of a [C][ncols] weight matrix (0 when C > 256:
+// the GEMM then reads the weights directly), and one launch packing W_qkv
+// ([C][3C]) into pk_qkv and W_proj ([C][C]) into pk_proj.
+size_t block_wpack_bytes(int C, int ncols, int dtype);
+hipError_t launch_block_wpack(const void *wqkv, const void *wproj, int C, int dtype, void *pk_qkv,
+                              void *pk_proj, hipStream_t stream);
 
 // Head widths with a tiled instantiation: the multiples of 4 from 8 to 32
 // (Dehazeformer's 12 and 16, Uformer's 32) and SwinIR's 30.

@@ -261,11 +261,25 @@ def test_noalloc_rejects_more_than_its_scratch(L):
     assert f(q, k, v, o, 0, 6, N_, d_, m_, 0, None, None) == OK
 
 
+def packed_weight_bytes(C, ncols, bf16):
+    """The GEMM's packed image of a [C][ncols] weight: one LDS tile image per
+    64 columns (fp32 [KP][68] words, bf16 [64][KP + 8] halves), KP the
+    contraction padded to 32, 64, 128, 192 or 256; none past C = 256."""
+    kp = next((x for x in (32, 64, 128, 192, 256) if C <= x), None)
+    if kp is None:
+        return 0
+    words = 32 * (kp + 8) if bf16 else kp * 68
+    return -(-ncols // 64) * words * 4
+
+
 def test_block_workspace_size():
     one = 16 * 16 * 96 * 4                      # one of Q, K, V, O in fp32 (256-byte multiple)
-    assert B.nystra_block_workspace_size(bshape(), 16) == 4 * one
-    assert B.nystra_block_workspace_size(bshape(), 16, B.BF16) == 2 * one
-    assert B.nystra_block_workspace_size(bshape(shift=4), 16, attention=B.BLOCK_EXACT) == 4 * one
+    pk32 = packed_weight_bytes(96, 288, False) + packed_weight_bytes(96, 96, False)
+    pk16 = packed_weight_bytes(96, 288, True) + packed_weight_bytes(96, 96, True)
+    assert pk32 % 256 == 0 and pk16 % 256 == 0
+    assert B.nystra_block_workspace_size(bshape(), 16) == 4 * one + pk32
+    assert B.nystra_block_workspace_size(bshape(), 16, B.BF16) == 2 * one + pk16
+    assert B.nystra_block_workspace_size(bshape(shift=4), 16, attention=B.BLOCK_EXACT) == 4 * one + pk32
     assert B.nystra_block_workspace_size(bshape(batch=0), 16) == 0
     # a whole-map window takes the token-split attention, whose workspace comes on top
     glob = bshape(height=128, width=128, channels=64, heads=2, window=128)
