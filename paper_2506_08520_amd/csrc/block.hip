@@ -34,6 +34,7 @@ struct BlockArgs {
     const void *wpk;              // wt packed as the register-resident kernel's LDS tiles
     const void *bias;             // [ncols] or null
     void *out0, *out1, *out2;     // Q, K, V (QKV) or Y (PROJ)
+    bool pair;                    // register-resident kernel: store adjacent column pairs
 };
 
 // Flat pixel (b H + y) W + x of token t of window `win`.
@@ -283,14 +284,18 @@ __global__ void __launch_bounds__(256) block_wpack_kernel(WPackArgs p)
             return __float_as_uint(W[int64_t(k) * ncols + n]);
     };
     uint32_t out;
+    int64_t dw = wi;   // destination word
     if constexpr (E::bytes == 2) {
-        const int h = 2 * w, n = h / L::PH, k = h - n * L::PH;   // PH even: one row
+        // consecutive threads take consecutive columns n (coalesced reads of
+        // two rows of W) and write the word holding k, k + 1 of column n
+        const int n = w & 63, k = 2 * (w >> 6);
         out = k < KP ? elem(k, n0 + n) | (elem(k + 1, n0 + n) << 16) : 0u;
+        dw = int64_t(ct) * L::tile + n * (L::PH / 2) + (k >> 1);
     } else {
         const int k = w / L::PF, r = w - k * L::PF;
         out = r < 64 ? elem(k, n0 + 16 * (r & 3) + (r >> 2)) : 0u;
     }
-    (second ? p.d1 : p.d0)[wi] = out;
+    (second ? p.d1 : p.d0)[dw] = out;
 }
 
 template <class E, bool PROJ, int KP>
@@ -474,25 +479,60 @@ __global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs 
         }
         // Epilogue: lane (g, c) holds rows 4g + i of the wave's 16, column c of tile q;
         // destination = row part (per lane, computed once) + column part (table).
+        // With a.pair, lanes c and c ^ 1 swap one value per two rows so that the
+        // even lane holds columns (c, c + 1) of row 4g + 2p and the odd lane
+        // those of row 4g + 2p + 1: one 4-byte (bf16) or 8-byte (fp32) store per
+        // two outputs.  Pairs never straddle a head or Q/K/V (d_h and C even).
+        if (a.pair) {
+            const bool odd = c & 1;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int n = 64 * ct + 16 * q + c;
-            if (n >= a.ncols)
-                continue;
-            const float bias = colbias[n];
-            const uint32_t col = uint32_t(coltab[it & 1][16 * q + c]);
-            const int which = colwhich[it & 1][16 * q + c];
-            typename E::T *dst = static_cast<typename E::T *>(which == 0 ? a.out0
-                                                              : which == 1 ? a.out1 : a.out2);
+            for (int q = 0; q < 4; ++q) {
+                const int n = 64 * ct + 16 * q + c;   // n and n ^ 1 lie on one side of ncols
+                if (n >= a.ncols)
+                    continue;
+                const float bias = colbias[n];
+                const int cp = (16 * q + c) & ~1;
+                const uint32_t col = uint32_t(coltab[it & 1][cp]);
+                const int which = colwhich[it & 1][cp];
+                typename E::T *dst = static_cast<typename E::T *>(which == 0 ? a.out0
+                                                                  : which == 1 ? a.out1 : a.out2);
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                if (rowok[i]) {
-                    const float v = acc[q][i] + bias;
-                    if constexpr (BF)
-                        dst[rowoff[i] + col] = uint16_t(cvt_bf16x2(v, 0.f));   // RNE
-                    else
-                        dst[rowoff[i] + col] = v;
+                for (int pp = 0; pp < 2; ++pp) {
+                    const float v0 = acc[q][2 * pp] + bias, v1 = acc[q][2 * pp + 1] + bias;
+                    const float recv = dpp_xor1(odd ? v0 : v1);
+                    const float lo = odd ? recv : v0, hi = odd ? v1 : recv;
+                    const int i = 2 * pp + (odd ? 1 : 0);
+                    if (rowok[i]) {
+                        if constexpr (BF)
+                            *reinterpret_cast<uint32_t *>(dst + (rowoff[i] + col)) =
+                                cvt_bf16x2(lo, hi);   // RNE
+                        else
+                            *reinterpret_cast<float2 *>(dst + (rowoff[i] + col)) =
+                                make_float2(lo, hi);
+                    }
                 }
+            }
+        } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int n = 64 * ct + 16 * q + c;
+                if (n >= a.ncols)
+                    continue;
+                const float bias = colbias[n];
+                const uint32_t col = uint32_t(coltab[it & 1][16 * q + c]);
+                const int which = colwhich[it & 1][16 * q + c];
+                typename E::T *dst = static_cast<typename E::T *>(which == 0 ? a.out0
+                                                                  : which == 1 ? a.out1 : a.out2);
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (rowok[i]) {
+                        const float v = acc[q][i] + bias;
+                        if constexpr (BF)
+                            dst[rowoff[i] + col] = uint16_t(cvt_bf16x2(v, 0.f));   // RNE
+                        else
+                            dst[rowoff[i] + col] = v;
+                    }
+            }
         }
         if (more) {
             wstash((it + 1) & 1);
@@ -524,16 +564,21 @@ bool try_rk(const BlockArgs &a, hipStream_t stream)
     // never straddles two heads); the A base 4-byte aligned
     if (uintptr_t(a.a) % 4 != 0 || (E::bytes == 2 && (a.C % 2 != 0 || (PROJ && a.dh % 2 != 0))))
         return false;
+    // paired column stores: even widths, outputs aligned to two elements
+    BlockArgs b = a;
+    const uintptr_t al = 2 * E::bytes;
+    b.pair = a.ncols % 2 == 0 && a.dh % 2 == 0 && uintptr_t(a.out0) % al == 0 &&
+             (PROJ || (uintptr_t(a.out1) % al == 0 && uintptr_t(a.out2) % al == 0));
     if (a.C <= 32)
-        launch_rk<E, PROJ, 32>(a, stream);
+        launch_rk<E, PROJ, 32>(b, stream);
     else if (a.C <= 64)
-        launch_rk<E, PROJ, 64>(a, stream);
+        launch_rk<E, PROJ, 64>(b, stream);
     else if (a.C <= 128)
-        launch_rk<E, PROJ, 128>(a, stream);
+        launch_rk<E, PROJ, 128>(b, stream);
     else if (a.C <= 192)
-        launch_rk<E, PROJ, 192>(a, stream);
+        launch_rk<E, PROJ, 192>(b, stream);
     else if (a.C <= 256)
-        launch_rk<E, PROJ, 256>(a, stream);
+        launch_rk<E, PROJ, 256>(b, stream);
     else
         return false;
     return true;
@@ -648,6 +693,7 @@ hipError_t launch_block_gemm(const BlockGemm &g, hipStream_t stream)
     a.out0 = g.out0;
     a.out1 = g.out1;
     a.out2 = g.out2;
+    a.pair = false;
     if (g.dtype == 0)
         g.proj ? launch_gemm<F32, true>(a, stream) : launch_gemm<F32, false>(a, stream);
     else
