@@ -255,8 +255,8 @@ struct RkLds {
 // after another: bf16 [n][k] with pitch PH (element (k, n0 + n) at n PH + k),
 // fp32 [k][PF] with the four 16-column tiles' values of column c at 4c + t
 // (element (k, n0 + 16t + c)).  Every slot outside W (k >= C, n >= ncols, the
-// pitch padding) is zero.  One thread per 4-byte word; the second matrix's
-// words follow the first's in the grid.
+// pitch padding) is zero.  The second matrix's pieces follow the first's in
+// the grid.
 struct WPackArgs {
     const void *w0, *w1;   // W_qkv [C][3C], W_proj [C][C]
     uint32_t *d0, *d1;     // their packed images
@@ -266,15 +266,19 @@ struct WPackArgs {
 template <class E, int KP>
 __global__ void __launch_bounds__(256) block_wpack_kernel(WPackArgs p)
 {
+    // One thread per 16-byte piece of the images (four words).
     using L = RkLds<E, KP>;
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    constexpr int kPieces = L::tile / 4;   // per tile
     const int64_t gi = int64_t(blockIdx.x) * 256 + threadIdx.x;
-    const bool second = gi >= p.words0;
-    const int64_t wi = second ? gi - p.words0 : gi;
-    if (wi >= (second ? p.words1 : p.words0))
+    const int64_t p0 = p.words0 / 4;
+    const bool second = gi >= p0;
+    const int64_t pi = second ? gi - p0 : gi;
+    if (pi >= (second ? p.words1 / 4 : p0))
         return;
     const int ncols = second ? p.C : 3 * p.C;
     const typename E::T *W = static_cast<const typename E::T *>(second ? p.w1 : p.w0);
-    const int ct = int(wi / L::tile), w = int(wi - int64_t(ct) * L::tile), n0 = 64 * ct;
+    const int ct = int(pi / kPieces), r = int(pi - int64_t(ct) * kPieces), n0 = 64 * ct;
     auto elem = [&](int k, int n) -> uint32_t {
         if (k >= p.C || n >= ncols)
             return 0u;
@@ -283,19 +287,28 @@ __global__ void __launch_bounds__(256) block_wpack_kernel(WPackArgs p)
         else
             return __float_as_uint(W[int64_t(k) * ncols + n]);
     };
-    uint32_t out;
-    int64_t dw = wi;   // destination word
+    u32x4 out;
+    int dst;   // piece index within the tile image
     if constexpr (E::bytes == 2) {
-        // consecutive threads take consecutive columns n (coalesced reads of
-        // two rows of W) and write the word holding k, k + 1 of column n
-        const int n = w & 63, k = 2 * (w >> 6);
-        out = k < KP ? elem(k, n0 + n) | (elem(k + 1, n0 + n) << 16) : 0u;
-        dw = int64_t(ct) * L::tile + n * (L::PH / 2) + (k >> 1);
+        // column n = r mod 64 (consecutive threads: consecutive columns of
+        // eight rows of W), halves k0 .. k0 + 7 of its image row
+        const int n = r & 63, k0 = 8 * (r >> 6);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int k = k0 + 2 * e;
+            out[e] = k < KP ? elem(k, n0 + n) | (elem(k + 1, n0 + n) << 16) : 0u;
+        }
+        dst = (n * L::PH + k0) / 8;
     } else {
-        const int k = w / L::PF, r = w - k * L::PF;
-        out = r < 64 ? elem(k, n0 + 16 * (r & 3) + (r >> 2)) : 0u;
+        // row k, column c: the four 16-column tiles' values (slot 16 of a row
+        // is the pitch padding)
+        const int k = r / (L::PF / 4), c = r - k * (L::PF / 4);
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            out[t] = c < 16 ? elem(k, n0 + 16 * t + c) : 0u;
+        dst = r;
     }
-    (second ? p.d1 : p.d0)[dw] = out;
+    reinterpret_cast<u32x4 *>(second ? p.d1 : p.d0)[int64_t(ct) * kPieces + dst] = out;
 }
 
 template <class E, bool PROJ, int KP>
@@ -634,9 +647,9 @@ size_t block_wpack_bytes(int C, int ncols, int dtype)
 template <class E, int KP>
 void launch_wpack_k(const WPackArgs &p, hipStream_t stream)
 {
-    const int64_t words = int64_t(p.words0) + p.words1;
-    hipLaunchKernelGGL((block_wpack_kernel<E, KP>), dim3(unsigned((words + 255) / 256)), dim3(256),
-                       0, stream, p);
+    const int64_t pieces = (int64_t(p.words0) + p.words1) / 4;   // tiles are whole pieces
+    hipLaunchKernelGGL((block_wpack_kernel<E, KP>), dim3(unsigned((pieces + 255) / 256)),
+                       dim3(256), 0, stream, p);
 }
 
 template <class E>
