@@ -279,13 +279,17 @@ __global__ void __launch_bounds__(256) block_wpack_kernel(WPackArgs p)
     const int ncols = second ? p.C : 3 * p.C;
     const typename E::T *W = static_cast<const typename E::T *>(second ? p.w1 : p.w0);
     const int ct = int(pi / kPieces), r = int(pi - int64_t(ct) * kPieces), n0 = 64 * ct;
+    // Branch-free: every load reads an in-bounds element (indices clamped) and
+    // a select zeroes the slots outside W, so a thread's loads issue together.
     auto elem = [&](int k, int n) -> uint32_t {
-        if (k >= p.C || n >= ncols)
-            return 0u;
+        const bool ok = k < p.C && n < ncols;
+        const int64_t i = int64_t(k < p.C ? k : p.C - 1) * ncols + (n < ncols ? n : ncols - 1);
+        uint32_t x;
         if constexpr (E::bytes == 2)
-            return uint32_t(reinterpret_cast<const uint16_t *>(W)[int64_t(k) * ncols + n]);
+            x = uint32_t(reinterpret_cast<const uint16_t *>(W)[i]);
         else
-            return __float_as_uint(W[int64_t(k) * ncols + n]);
+            x = __float_as_uint(W[i]);
+        return ok ? x : 0u;
     };
     u32x4 out;
     int dst;   // piece index within the tile image
@@ -296,7 +300,7 @@ __global__ void __launch_bounds__(256) block_wpack_kernel(WPackArgs p)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int k = k0 + 2 * e;
-            out[e] = k < KP ? elem(k, n0 + n) | (elem(k + 1, n0 + n) << 16) : 0u;
+            out[e] = elem(k, n0 + n) | (elem(k + 1, n0 + n) << 16);   // zero from k = C on
         }
         dst = (n * L::PH + k0) / 8;
     } else {
