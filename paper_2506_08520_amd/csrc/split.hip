@@ -83,16 +83,28 @@ split_pool_kernel(const typename E::T *__restrict__ q, const typename E::T *__re
     for (int s = 0; s < 8; ++s)
         qs[s] = ks[s] = 0.f;
     // Wave w takes 16-token tiles w, w + 4, ... of the piece; four tiles per
-    // step so that their loads are in flight together.
+    // step so that their loads are in flight together.  When patch rows and
+    // pieces are whole tiles (pc and the piece length multiples of 16), a
+    // tile is 16 consecutive tokens of one patch row: its position is
+    // computed once per tile (uniform, scalar) instead of per lane.
+    const bool whole_tiles = a.pc % 16 == 0 && a.piece_len % 16 == 0;   // uniform
     for (int b = i0 + 16 * w; b < i1; b += 4 * 16 * kWaves) {
         float x[4][8], y[4][8];
         bool ok[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            const int i = b + 16 * kWaves * u + c;
-            ok[u] = i < i1;
-            const int ii = ok[u] ? i : i0;
-            const int64_t t = int64_t(r0 + ii / a.pc) * a.cols + c0 + ii % a.pc;
+            int64_t t;
+            if (whole_tiles) {
+                const int ib = b + 16 * kWaves * u;   // tile start, uniform
+                ok[u] = ib < i1;
+                const int ii = ok[u] ? ib : i0;
+                t = int64_t(r0 + ii / a.pc) * a.cols + c0 + ii % a.pc + c;
+            } else {
+                const int i = b + 16 * kWaves * u + c;
+                ok[u] = i < i1;
+                const int ii = ok[u] ? i : i0;
+                t = int64_t(r0 + ii / a.pc) * a.cols + c0 + ii % a.pc;
+            }
             load_chunk8<E, D>(qu + t * D, g, x[u]);
             load_chunk8<E, D>(ku + t * D, g, y[u]);
         }
