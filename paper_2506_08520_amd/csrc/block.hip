@@ -35,6 +35,7 @@ struct BlockArgs {
     const void *bias;             // [ncols] or null
     void *out0, *out1, *out2;     // Q, K, V (QKV) or Y (PROJ)
     bool pair;                    // register-resident kernel: store adjacent column pairs
+    int64_t ostride;              // register-resident kernel: elements from Q to K and K to V
 };
 
 // Flat pixel (b H + y) W + x of token t of window `win`.
@@ -417,12 +418,12 @@ __global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs 
                 dst[idx] = wr[j];
         }
     };
-    // Column part of the destination for the 64 columns of the current tile:
-    // which output tensor, and (QKV) head h, feature f -> h N d_h + f.  The
-    // bias of every column is staged in LDS once: a global load in the
-    // epilogue would wait behind the next tile's W pieces in flight.
-    __shared__ int coltab[2][64];
-    __shared__ int colwhich[2][64];
+    // Column part of the destination for the 64 columns of the current tile,
+    // from out0: (QKV) output tensor `which` at which * ostride, head h,
+    // feature f -> h N d_h + f; (PROJ) the column.  The bias of every column
+    // is staged in LDS once: a global load in the epilogue would wait behind
+    // the next tile's W pieces in flight.
+    __shared__ uint32_t coltab[2][64];
     __shared__ float colbias[3 * 256];
     for (int n = tid; n < a.ncols; n += 64 * kRkWaves)
         colbias[n] = a.bias ? ld<E>(a.bias, n) : 0.f;
@@ -436,8 +437,7 @@ __global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs 
                 const int hh = cc / a.dh;
                 col = hh * a.N * a.dh + (cc - hh * a.dh);
             }
-            coltab[buf][tid] = col;
-            colwhich[buf][tid] = which;
+            coltab[buf][tid] = uint32_t(which * a.ostride + col);
         }
     };
 
@@ -509,10 +509,8 @@ __global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs 
                     continue;
                 const float bias = colbias[n];
                 const int cp = (16 * q + c) & ~1;
-                const uint32_t col = uint32_t(coltab[it & 1][cp]);
-                const int which = colwhich[it & 1][cp];
-                typename E::T *dst = static_cast<typename E::T *>(which == 0 ? a.out0
-                                                                  : which == 1 ? a.out1 : a.out2);
+                const uint32_t col = coltab[it & 1][cp];
+                typename E::T *dst = static_cast<typename E::T *>(a.out0);
 #pragma unroll
                 for (int pp = 0; pp < 2; ++pp) {
                     const float v0 = acc[q][2 * pp] + bias, v1 = acc[q][2 * pp + 1] + bias;
@@ -536,10 +534,8 @@ __global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs 
                 if (n >= a.ncols)
                     continue;
                 const float bias = colbias[n];
-                const uint32_t col = uint32_t(coltab[it & 1][16 * q + c]);
-                const int which = colwhich[it & 1][16 * q + c];
-                typename E::T *dst = static_cast<typename E::T *>(which == 0 ? a.out0
-                                                                  : which == 1 ? a.out1 : a.out2);
+                const uint32_t col = coltab[it & 1][16 * q + c];
+                typename E::T *dst = static_cast<typename E::T *>(a.out0);
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
                     if (rowok[i]) {
@@ -581,8 +577,20 @@ bool try_rk(const BlockArgs &a, hipStream_t stream)
     // never straddles two heads); the A base 4-byte aligned
     if (uintptr_t(a.a) % 4 != 0 || (E::bytes == 2 && (a.C % 2 != 0 || (PROJ && a.dh % 2 != 0))))
         return false;
-    // paired column stores: even widths, outputs aligned to two elements
+    // One output base: Q, K, V at a uniform element stride from out0, every
+    // offset under 2^32 elements.
     BlockArgs b = a;
+    b.ostride = 0;
+    if constexpr (!PROJ) {
+        const int64_t s1 = static_cast<const char *>(a.out1) - static_cast<const char *>(a.out0);
+        const int64_t s2 = static_cast<const char *>(a.out2) - static_cast<const char *>(a.out1);
+        if (s1 != s2 || s1 < 0 || s1 % E::bytes != 0)
+            return false;
+        b.ostride = s1 / E::bytes;
+        if (3 * b.ostride >= (int64_t(1) << 32) || b.ostride < a.rows * int64_t(a.C))
+            return false;
+    }
+    // paired column stores: even widths, outputs aligned to two elements
     const uintptr_t al = 2 * E::bytes;
     b.pair = a.ncols % 2 == 0 && a.dh % 2 == 0 && uintptr_t(a.out0) % al == 0 &&
              (PROJ || (uintptr_t(a.out1) % al == 0 && uintptr_t(a.out2) % al == 0));
@@ -711,6 +719,7 @@ hipError_t launch_block_gemm(const BlockGemm &g, hipStream_t stream)
     a.out1 = g.out1;
     a.out2 = g.out2;
     a.pair = false;
+    a.ostride = 0;
     if (g.dtype == 0)
         g.proj ? launch_gemm<F32, true>(a, stream) : launch_gemm<F32, false>(a, stream);
     else
