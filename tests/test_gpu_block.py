@@ -89,3 +89,29 @@ def test_block_deterministic():
     a = run_block(inputs, 6, 8, 4, 16, "f32", "nystrom")
     b = run_block(inputs, 6, 8, 4, 16, "f32", "nystrom")
     assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_block_weights_repacked_every_call(dtype):
+    """The GEMMs read the weights from a packed copy in the workspace, written
+    by each call: a second call with other weights on the same workspace must
+    give the second weights' block, not the first's."""
+    C, heads, w, s, m = 96, 3, 8, 4, 16
+    first = W.block_inputs(1, 16, 16, C, seed=11, dtype=dtype)
+    second = W.block_inputs(1, 16, 16, C, seed=12, dtype=dtype)
+    x = to_dev(first[0], dtype)
+    shape = B.BlockShape(1, 16, 16, C, heads, w, s)
+    code = B.F32 if dtype == "f32" else B.BF16
+    ws = torch.empty(B.nystra_block_workspace_size(shape, m, code), dtype=torch.uint8,
+                     device="cuda")
+    ys = []
+    for inp in (first, second):
+        wq, bq, wp, bp = (to_dev(a, dtype) for a in inp[1:])
+        ys.append(to_host(B.nystra_block_forward(x, wq, bq, wp, bp, heads, w, shift=s, m=m,
+                                                 workspace=ws)))
+    torch.cuda.synchronize()
+    for seed, inp, y in zip((11, 12), (first, second), ys):
+        ref = OB.block_forward(first[0], *inp[1:], heads=heads, window=w, shift=s, m=m,
+                               dtype=dtype, round_output=False)
+        check(y, ref, dtype, f"block with the weights of seed {seed}",
+              beyond_bar=BLOCK_BEYOND_BF16)
