@@ -316,6 +316,15 @@ __global__ void __launch_bounds__(256) block_wpack_kernel(WPackArgs p)
     reinterpret_cast<u32x4 *>(second ? p.d1 : p.d0)[int64_t(ct) * kPieces + dst] = out;
 }
 
+// Words per batch of the A stage: the largest divisor of n up to 16.
+constexpr int stage_batch(int n)
+{
+    for (int b = 16; b > 1; --b)
+        if (n % b == 0)
+            return b;
+    return 1;
+}
+
 template <class E, bool PROJ, int KP>
 __global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs a)
 {
@@ -359,14 +368,33 @@ __global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs 
     }
     __syncthreads();
     {
+        // Each thread copies kPerT words, in batches whose loads are all in
+        // flight before the first is waited for (a loop of load, wait, store
+        // would chain kPerT memory round trips).
+        constexpr int kPerT = kRkRows * AWL / (64 * kRkWaves);
+        constexpr int kBatch = stage_batch(kPerT);
+        static_assert(kPerT * 64 * kRkWaves == kRkRows * AWL, "whole words per thread");
         const uint32_t *src = static_cast<const uint32_t *>(a.a);
-        for (int j = tid; j < kRkRows * AWL; j += 64 * kRkWaves) {
-            const int row = j / AWL, w = j - row * AWL;
-            const int rb = rowbase[row], co = colofs[w];
-            const bool ok = rb >= 0 && co >= 0;
-            const int e = ok ? rb + co : 0;
-            const uint32_t x = src[BF ? e >> 1 : e];
-            reinterpret_cast<uint32_t *>(astage)[row * AP + w] = ok ? x : 0u;
+        uint32_t *dst = reinterpret_cast<uint32_t *>(astage);
+        for (int b0 = 0; b0 < kPerT; b0 += kBatch) {
+            uint32_t x[kBatch];
+            int at[kBatch];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int j = tid + (b0 + u) * 64 * kRkWaves;
+                const int row = j / AWL, w = j - row * AWL;
+                const int rb = rowbase[row], co = colofs[w];
+                const bool ok = rb >= 0 && co >= 0;
+                const int e = ok ? rb + co : 0;
+                x[u] = src[BF ? e >> 1 : e];
+                at[u] = ok ? row * AP + w : -1;
+            }
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int j = tid + (b0 + u) * 64 * kRkWaves;
+                const int row = j / AWL, w = j - row * AWL;
+                dst[row * AP + w] = at[u] >= 0 ? x[u] : 0u;
+            }
         }
     }
     __syncthreads();
@@ -494,6 +522,14 @@ __global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs 
                     acc[q] = mfma4(av[s], bv[q], acc[q]);
             }
         }
+        // The next tile goes to the idle buffer before this tile's stores are
+        // issued: the wait for its loads counts every earlier vector memory
+        // operation, stores included, so stashing after the stores would
+        // wait for their completion on every tile.
+        if (more) {
+            wstash((it + 1) & 1);
+            cfill(phys(it + 1), (it + 1) & 1);
+        }
         // Epilogue: lane (g, c) holds rows 4g + i of the wave's 16, column c of tile q;
         // destination = row part (per lane, computed once) + column part (table).
         // With a.pair, lanes c and c ^ 1 swap one value per two rows so that the
@@ -546,10 +582,6 @@ __global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs 
                             dst[rowoff[i] + col] = v;
                     }
             }
-        }
-        if (more) {
-            wstash((it + 1) & 1);
-            cfill(phys(it + 1), (it + 1) & 1);
         }
         __syncthreads();
     }
