@@ -366,6 +366,52 @@ __global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs 
         }
         colofs[w] = k < a.C ? off : -1;
     }
+    // ---- W tiles: the packed image of each 64-column tile (block_wpack_kernel
+    // lays it out exactly as the LDS tile below, padding included) is copied
+    // global -> registers -> LDS in 16-byte pieces, consecutive lanes taking
+    // consecutive pieces: coalesced loads, conflict-free stores, no index
+    // arithmetic per element.
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    constexpr int kPieces = L::tile / 4;   // 16-byte pieces of a tile image
+    constexpr int kPer = (kPieces + 64 * kRkWaves - 1) / (64 * kRkWaves);
+    u32x4 wr[kPer];
+    const int nct = (a.ncols + 63) / 64;
+    const u32x4 *wsrc = static_cast<const u32x4 *>(a.wpk);
+    auto wfetch = [&](int ct) {
+        const u32x4 *src = wsrc + int64_t(ct) * kPieces;
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) {   // past the image: re-read its last piece
+            const int idx = tid + j * 64 * kRkWaves;
+            wr[j] = src[idx < kPieces ? idx : kPieces - 1];
+        }
+    };
+    auto wstash = [&](int buf) {
+        u32x4 *dst = reinterpret_cast<u32x4 *>(wbuf(buf));
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) {
+            const int idx = tid + j * 64 * kRkWaves;
+            if (kPer * 64 * kRkWaves == kPieces || idx < kPieces)
+                dst[idx] = wr[j];
+        }
+    };
+    // Workgroups start at different column tiles, so that at any moment they
+    // read different tiles of W instead of all hitting the same L2 lines.
+    const int start = int(blockIdx.x % unsigned(nct));
+    auto phys = [&](int i) { return i + start < nct ? i + start : i + start - nct; };
+    // The first W tile and the bias are requested now, their latency hidden
+    // behind the A stage; the bias of every column is staged in LDS once (a
+    // global load in the epilogue would wait behind the next tile's W pieces
+    // in flight).
+    wfetch(phys(0));
+    __shared__ float colbias[3 * 256];
+    constexpr int kBiasPer = (3 * 256 + 64 * kRkWaves - 1) / (64 * kRkWaves);
+    float bz[kBiasPer];
+#pragma unroll
+    for (int j = 0; j < kBiasPer; ++j) {
+        const int n = tid + j * 64 * kRkWaves;
+        const int nc = n < a.ncols ? n : a.ncols - 1;
+        bz[j] = a.bias ? ld<E>(a.bias, nc) : 0.f;
+    }
     __syncthreads();
     {
         // Each thread copies kPerT words, in batches whose loads are all in
@@ -418,43 +464,12 @@ __global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs 
     }
     __syncthreads();   // the stage becomes the W tiles
 
-    // ---- W tiles: the packed image of each 64-column tile (block_wpack_kernel
-    // lays it out exactly as the LDS tile below, padding included) is copied
-    // global -> registers -> LDS in 16-byte pieces, consecutive lanes taking
-    // consecutive pieces: coalesced loads, conflict-free stores, no index
-    // arithmetic per element.
-    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-    constexpr int kPieces = L::tile / 4;   // 16-byte pieces of a tile image
-    constexpr int kPer = (kPieces + 64 * kRkWaves - 1) / (64 * kRkWaves);
-    u32x4 wr[kPer];
-    const int nct = (a.ncols + 63) / 64;
-    const u32x4 *wsrc = static_cast<const u32x4 *>(a.wpk);
-    auto wfetch = [&](int ct) {
-        const u32x4 *src = wsrc + int64_t(ct) * kPieces;
-#pragma unroll
-        for (int j = 0; j < kPer; ++j) {   // past the image: re-read its last piece
-            const int idx = tid + j * 64 * kRkWaves;
-            wr[j] = src[idx < kPieces ? idx : kPieces - 1];
-        }
-    };
-    auto wstash = [&](int buf) {
-        u32x4 *dst = reinterpret_cast<u32x4 *>(wbuf(buf));
-#pragma unroll
-        for (int j = 0; j < kPer; ++j) {
-            const int idx = tid + j * 64 * kRkWaves;
-            if (kPer * 64 * kRkWaves == kPieces || idx < kPieces)
-                dst[idx] = wr[j];
-        }
-    };
     // Column part of the destination for the 64 columns of the current tile,
     // from out0: (QKV) output tensor `which` at which * ostride, head h,
     // feature f -> h N d_h + f; (PROJ) the column.  The bias of every column
     // is staged in LDS once: a global load in the epilogue would wait behind
     // the next tile's W pieces in flight.
     __shared__ uint32_t coltab[2][64];
-    __shared__ float colbias[3 * 256];
-    for (int n = tid; n < a.ncols; n += 64 * kRkWaves)
-        colbias[n] = a.bias ? ld<E>(a.bias, n) : 0.f;
     auto cfill = [&](int ct, int buf) {
         if (tid < 64) {
             const int n = 64 * ct + tid;
@@ -485,11 +500,12 @@ __global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs 
                                   : int64_t(wn) * a.N * a.C + int64_t(tt) * a.dh);
     }
 
-    // Workgroups start at different column tiles, so that at any moment they
-    // read different tiles of W instead of all hitting the same L2 lines.
-    const int start = int(blockIdx.x % unsigned(nct));
-    auto phys = [&](int i) { return i + start < nct ? i + start : i + start - nct; };
-    wfetch(phys(0));
+#pragma unroll
+    for (int j = 0; j < kBiasPer; ++j) {
+        const int n = tid + j * 64 * kRkWaves;
+        if (n < a.ncols)
+            colbias[n] = bz[j];
+    }
     wstash(0);
     cfill(phys(0), 0);
     __syncthreads();
