@@ -156,16 +156,21 @@ __global__ void __launch_bounds__(64) split_bar_kernel(SplitArgs a)
     const int half = threadIdx.x >> 5, f = threadIdx.x & 31;
     float acc = 0.f;
     if (l < a.m && f < a.d) {
+        // eight pieces per step, their loads in flight together (the last
+        // step's missing pieces read piece `half` and add zero)
         const float *p = a.part + (uw * a.m + l) * int64_t(a.pieces) * kWP + f;
-        float acc2 = 0.f;
-        int r = half;
-        for (; r + 2 < a.pieces; r += 4) {
-            acc += p[int64_t(r) * kWP];
-            acc2 += p[int64_t(r + 2) * kWP];
+        for (int r0 = half; r0 < a.pieces; r0 += 16) {
+            float x[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int r = r0 + 2 * u;
+                const float y = p[int64_t(r < a.pieces ? r : half) * kWP];
+                x[u] = r < a.pieces ? y : 0.f;
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                acc += x[u];
         }
-        if (r < a.pieces)
-            acc += p[int64_t(r) * kWP];
-        acc += acc2;
     }
     acc += __shfl_xor(acc, 32, 64);
     if (half == 0)
@@ -453,15 +458,19 @@ split_keys_kernel(const typename E::T *__restrict__ k, const typename E::T *__re
 
 // ---- C: merge of the chunk records ------------------------------------------
 // Block (unit, landmark tile j, column group q): q < 8 merges features
-// 4q .. 4q+3 of T, q = 8 the column T_D.  Four slices of 64 threads take every
-// fourth chunk; thread (landmark li, column x) of a slice keeps a running
-// maximum and the sum against it, eight chunk records in flight per step, and
-// the slices are merged in LDS in a fixed order.  Every block of a tile
-// computes the same maxima (a max is exact); block q = 0 stores s2 * m_U.
-__global__ void __launch_bounds__(256) split_merge_kernel(SplitArgs a, int MT)
+// 4q .. 4q+3 of T, q = 8 the column T_D.  kMergeSlices slices of 64 threads
+// take every kMergeSlices-th chunk; thread (landmark li, column x) of a slice
+// keeps a running maximum and the sum against it, eight chunk records in
+// flight per step (the last step's missing records read as maximum -inf,
+// weight 0), and the slices are merged in LDS in a fixed order.  Every block
+// of a tile computes the same maxima (a max is exact); block q = 0 stores
+// s2 * m_U.
+constexpr int kMergeSlices = 16;
+
+__global__ void __launch_bounds__(64 * kMergeSlices) split_merge_kernel(SplitArgs a, int MT)
 {
-    constexpr int kU = 8;
-    __shared__ float smax[4][64], ssum[4][64];
+    constexpr int kU = 8, S = kMergeSlices;
+    __shared__ float smax[S][64], ssum[S][64];
     const int per_unit = MT * kMergeGroups;
     const int64_t unit = blockIdx.x / per_unit;
     const int rem = int(blockIdx.x - unit * per_unit);
@@ -473,14 +482,17 @@ __global__ void __launch_bounds__(256) split_merge_kernel(SplitArgs a, int MT)
     const int dst = q < kMergeGroups - 1 ? l * kWP + 4 * q + x : kRecD + l;         // merged
     const float *rec = a.rec + unit * a.nchunk * kRec;
     float mx = -INFINITY, sum = 0.f;
-    int ch = slice;
-    for (; ch + 4 * (kU - 1) < a.nchunk; ch += 4 * kU) {
+    // A step starts at a chunk below nchunk, so its maximum is finite.
+    for (int ch = slice; ch < a.nchunk; ch += S * kU) {
         float cm[kU], cv[kU];
 #pragma unroll
         for (int u = 0; u < kU; ++u) {
-            const float *r = rec + int64_t(ch + 4 * u) * kRec;
-            cm[u] = r[kRecM + l];
-            cv[u] = r[col];
+            const int c = ch + S * u;
+            const bool ok = c < a.nchunk;
+            const float *r = rec + int64_t(ok ? c : ch) * kRec;
+            const float m = r[kRecM + l], v = r[col];
+            cm[u] = ok ? m : -INFINITY;
+            cv[u] = ok ? v : 0.f;
         }
         float nm = mx;
 #pragma unroll
@@ -492,23 +504,17 @@ __global__ void __launch_bounds__(256) split_merge_kernel(SplitArgs a, int MT)
             sum = fmaf(fast_exp2(a.s2 * (cm[u] - nm)), cv[u], sum);
         mx = nm;
     }
-    for (; ch < a.nchunk; ch += 4) {
-        const float *r = rec + int64_t(ch) * kRec;
-        const float cm = r[kRecM + l], nm = fmaxf(mx, cm);
-        sum = fmaf(fast_exp2(a.s2 * (cm - nm)), r[col], sum * fast_exp2(a.s2 * (mx - nm)));
-        mx = nm;
-    }
     smax[slice][t] = mx;
     ssum[slice][t] = sum;
     __syncthreads();
     if (slice == 0) {
         float M = mx;
 #pragma unroll
-        for (int s = 1; s < 4; ++s)
+        for (int s = 1; s < S; ++s)
             M = fmaxf(M, smax[s][t]);
         float tot = 0.f;
 #pragma unroll
-        for (int s = 0; s < 4; ++s)   // a slice without chunks has max -inf and weight 0
+        for (int s = 0; s < S; ++s)   // a slice without chunks has max -inf and weight 0
             tot += fast_exp2(a.s2 * (smax[s][t] - M)) * ssum[s][t];
         float *cb = a.comb + unit * kRec;
         cb[dst] = tot;
@@ -837,8 +843,8 @@ void launch_split_md(const Problem &p, const Plan &s, const SplitArgs &a, hipStr
     else
         hipLaunchKernelGGL((split_keys_kernel<E, MT, D, false>), dim3(U * unsigned(s.nchunk)),
                            block, 0, stream, k, v, a);
-    hipLaunchKernelGGL(split_merge_kernel, dim3(U * unsigned(MT * kMergeGroups)), dim3(256), 0,
-                       stream, a, MT);
+    hipLaunchKernelGGL(split_merge_kernel, dim3(U * unsigned(MT * kMergeGroups)),
+                       dim3(64 * kMergeSlices), 0, stream, a, MT);
     const size_t lds = size_t(LargeLds<MT>::total) * sizeof(float);
     if (bfm)
         hipLaunchKernelGGL((split_core_kernel<MT, D, E::bytes == 2>), dim3(U), dim3(64 * MT), lds,
