@@ -366,6 +366,13 @@ def block_bench(args):
             res[f"block_{key}_us"] = round(timed(lambda: B.nystra_block_forward(
                 x, wq, bq, wp, bp, heads, w, shift=shift, m=m, attention=att, workspace=ws,
                 out=y), reps if key == "nystrom" or w <= 32 else 3), 2)
+            if key == "nystrom":
+                # the weights packed once, as for inference (no per-call packing)
+                packed = B.nystra_block_pack_weights(wq.view(C, 3 * C), wp.view(C, C))
+                res["block_nystrom_prepacked_us"] = round(timed(lambda: B.nystra_block_forward(
+                    x, wq, bq, wp, bp, heads, w, shift=shift, m=m, attention=att, workspace=ws,
+                    out=y, packed=packed), reps), 2)
+                del packed
             del ws
         # the attention alone on window-partitioned tensors of the same size
         nw = (side // w) ** 2

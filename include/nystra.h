@@ -228,6 +228,34 @@ int nystra_block_forward(const void *X, const void *Wqkv, const void *bqkv, cons
                          int dtype, const nystra_opts *opts, int attention, void *workspace,
                          size_t workspace_bytes, void *stream);
 
+/* The block with its projection weights packed once (inference, where W_qkv
+ * and W_proj do not change between calls; the same Sec. 1 block as above).
+ * nystra_block_packed_size: host-only bytes of the packed image of W_qkv and
+ * W_proj for `channels` and `dtype` (0 for channels > 256, where the block
+ * reads the weights as given).
+ * nystra_block_pack_weights: enqueues on `stream` the packing of Wqkv
+ * [C][3C] and Wproj [C][C] (device, `dtype`, element-aligned) into `packed`
+ * (device, 256-byte aligned, at least that size, disjoint from the weights;
+ * caller-owned).  A no-op for channels > 256.
+ * nystra_block_forward_packed: nystra_block_forward with the packing step
+ * skipped: the GEMMs read `packed`, which must hold the image of the same
+ * Wqkv and Wproj for these channels and dtype (its contents are not checked;
+ * repack after changing the weights).  `packed` is required (NYSTRA_ERR_NULL)
+ * for channels <= 256, ignored above; 256-byte aligned (NYSTRA_ERR_ALIGN) and
+ * disjoint from Y and the workspace (NYSTRA_ERR_OVERLAP).  Every other
+ * argument, the workspace size included, is as for nystra_block_forward.
+ * Results are identical to nystra_block_forward's. */
+int nystra_block_packed_size(int channels, int dtype, size_t *bytes);
+
+int nystra_block_pack_weights(const void *Wqkv, const void *Wproj, int channels, int dtype,
+                              void *packed, size_t packed_bytes, void *stream);
+
+int nystra_block_forward_packed(const void *X, const void *Wqkv, const void *bqkv,
+                                const void *Wproj, const void *bproj, const void *packed,
+                                void *Y, const nystra_block_shape *shape, int m, int dtype,
+                                const nystra_opts *opts, int attention, void *workspace,
+                                size_t workspace_bytes, void *stream);
+
 /* Exact windowed softmax self-attention, Eq. (1), per unit:
  *   O = softmax(scale Q K^T) V, with the row maximum subtracted inside the
  *   softmax.  scale <= 0 selects 1/sqrt(d_h).  Same layout, limits and

@@ -23,6 +23,7 @@ EXPORTS = (
     "nystra_exact_attn_forward", "nystra_landmark_pool", "nystra_landmark_map",
     "nystra_select_variant", "nystra_attn_workspace_size", "nystra_attn_forward_ws",
     "nystra_block_workspace_size", "nystra_block_forward", "nystra_attn_forward_noalloc",
+    "nystra_block_packed_size", "nystra_block_pack_weights", "nystra_block_forward_packed",
     "nystra_status_str", "nystra_last_error",
 )
 STATIC_SCRATCH_BYTES = 32 << 20   # NYSTRA_STATIC_SCRATCH_BYTES
@@ -87,8 +88,14 @@ def lib():
                                                      ctypes.c_size_t, _vp])
     L.nystra_attn_forward_noalloc.argtypes = ([_vp] * 4 + [_i] * 6 +
                                               [ctypes.POINTER(Opts), _vp])
-    for name in EXPORTS[:12]:
-        getattr(L, name).restype = ctypes.c_int
+    L.nystra_block_packed_size.argtypes = [_i, _i, ctypes.POINTER(ctypes.c_size_t)]
+    L.nystra_block_pack_weights.argtypes = [_vp, _vp, _i, _i, _vp, ctypes.c_size_t, _vp]
+    L.nystra_block_forward_packed.argtypes = ([_vp] * 7 + [ctypes.POINTER(BlockShape), _i, _i,
+                                                           ctypes.POINTER(Opts), _i, _vp,
+                                                           ctypes.c_size_t, _vp])
+    for name in EXPORTS:
+        if name not in ("nystra_status_str", "nystra_last_error"):
+            getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
 
@@ -210,10 +217,12 @@ def nystra_block_workspace_size(shape, m, dtype=F32, opts=None, attention=BLOCK_
 
 def nystra_block_forward(x, w_qkv, b_qkv, w_proj, b_proj, heads, window, shift=0, m=16,
                          opts=None, attention=BLOCK_NYSTROM, workspace=None, out=None,
-                         stream=None):
+                         stream=None, packed=None):
     """Window-attention block on x [B, H, W, C] (device, contiguous); returns Y
     of the same shape.  Biases may be None.  The workspace is allocated from
-    torch's allocator when not given."""
+    torch's allocator when not given.  ``packed``: the image from
+    nystra_block_pack_weights of these weights (the per-call packing is then
+    skipped)."""
     import torch
     if x.dim() != 4 or not x.is_contiguous() or not x.is_cuda:
         raise ValueError("x must be a contiguous device tensor [B, H, W, C]")
@@ -229,11 +238,49 @@ def nystra_block_forward(x, w_qkv, b_qkv, w_proj, b_proj, heads, window, shift=0
     nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     y = torch.empty_like(x) if out is None else out
     po = ctypes.byref(opts) if opts is not None else None
-    rc = lib().nystra_block_forward(_ptr(x), _ptr(w_qkv), _ptr(b_qkv), _ptr(w_proj),
-                                    _ptr(b_proj), _ptr(y), ctypes.byref(shape), m, code, po,
-                                    attention, _ptr(workspace), nbytes, _stream(stream))
-    _check(rc, "nystra_block_forward")
+    if packed is None:
+        rc = lib().nystra_block_forward(_ptr(x), _ptr(w_qkv), _ptr(b_qkv), _ptr(w_proj),
+                                        _ptr(b_proj), _ptr(y), ctypes.byref(shape), m, code, po,
+                                        attention, _ptr(workspace), nbytes, _stream(stream))
+        _check(rc, "nystra_block_forward")
+    else:
+        rc = lib().nystra_block_forward_packed(_ptr(x), _ptr(w_qkv), _ptr(b_qkv), _ptr(w_proj),
+                                               _ptr(b_proj), _ptr(packed), _ptr(y),
+                                               ctypes.byref(shape), m, code, po, attention,
+                                               _ptr(workspace), nbytes, _stream(stream))
+        _check(rc, "nystra_block_forward_packed")
     return y
+
+
+def nystra_block_packed_size(channels, dtype=F32):
+    """Bytes of the packed W_qkv and W_proj image (0 for channels > 256)."""
+    n = ctypes.c_size_t(0)
+    _check(lib().nystra_block_packed_size(int(channels), dtype, ctypes.byref(n)),
+           "nystra_block_packed_size")
+    return n.value
+
+
+def nystra_block_pack_weights(w_qkv, w_proj, out=None, stream=None):
+    """Packs w_qkv [C, 3C] and w_proj [C, C] (device, contiguous, one dtype)
+    for nystra_block_forward(..., packed=); returns the uint8 image (None for
+    channels > 256, where the block reads the weights as given)."""
+    import torch
+    C = int(w_proj.shape[0])
+    for t in (w_qkv, w_proj):
+        if t.dtype != w_proj.dtype or not t.is_contiguous() or not t.is_cuda:
+            raise ValueError("weights must be contiguous device tensors of one dtype")
+    if tuple(w_qkv.shape) != (C, 3 * C) or tuple(w_proj.shape) != (C, C):
+        raise ValueError("expected w_qkv [C, 3C] and w_proj [C, C]")
+    code = _dtype_code(w_proj)
+    need = nystra_block_packed_size(C, code)
+    if need == 0:
+        return None
+    if out is None:
+        out = torch.empty(need, dtype=torch.uint8, device=w_proj.device)
+    rc = lib().nystra_block_pack_weights(_ptr(w_qkv), _ptr(w_proj), C, code, _ptr(out),
+                                         out.numel(), _stream(stream))
+    _check(rc, "nystra_block_pack_weights")
+    return out
 
 
 def nystra_exact_attn_forward(q, k, v, scale=0.0, out=None, stream=None):

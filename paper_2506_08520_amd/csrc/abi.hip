@@ -531,27 +531,22 @@ int plan_block(const nystra_block_shape *s, int m, int dtype, const nystra_opts 
     return NYSTRA_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-int nystra_block_workspace_size(const nystra_block_shape *shape, int m, int dtype,
-                                const nystra_opts *opts, int attention, size_t *bytes)
+// Bytes of the packed W_qkv and W_proj image (each part padded to 256 bytes;
+// 0 when channels > 256).
+size_t packed_parts(int C, int dtype, size_t *qkv_part)
 {
-    if (!bytes)
-        return NYSTRA_ERR_NULL;
-    BlockPlan bp;
-    const int rc = plan_block(shape, m, dtype, opts, attention, &bp);
-    if (rc != NYSTRA_OK)
-        return rc;
-    *bytes = shape->batch == 0 ? 0 : bp.bytes;
-    return NYSTRA_OK;
+    const size_t q = pad256(nystra::block_wpack_bytes(C, 3 * C, dtype));
+    *qkv_part = q;
+    return q + pad256(nystra::block_wpack_bytes(C, C, dtype));
 }
 
-int nystra_block_forward(const void *X, const void *Wqkv, const void *bqkv, const void *Wproj,
-                         const void *bproj, void *Y, const nystra_block_shape *shape, int m,
-                         int dtype, const nystra_opts *opts, int attention, void *workspace,
-                         size_t workspace_bytes, void *stream)
+// The block of nystra_block_forward.  With with_packed, the GEMMs read the
+// weight image at `packed` (required when channels <= 256, ignored above)
+// instead of packing W_qkv and W_proj into the workspace first.
+int block_forward(const void *X, const void *Wqkv, const void *bqkv, const void *Wproj,
+                  const void *bproj, bool with_packed, const void *packed, void *Y,
+                  const nystra_block_shape *shape, int m, int dtype, const nystra_opts *opts,
+                  int attention, void *workspace, size_t workspace_bytes, void *stream)
 {
     BlockPlan bp;
     int rc = plan_block(shape, m, dtype, opts, attention, &bp);
@@ -559,7 +554,8 @@ int nystra_block_forward(const void *X, const void *Wqkv, const void *bqkv, cons
         return rc;
     if (shape->batch == 0)
         return NYSTRA_OK;
-    if (!X || !Wqkv || !Wproj || !Y)
+    const bool use_packed = with_packed && bp.pk_qkv != 0;
+    if (!X || !Wqkv || !Wproj || !Y || (use_packed && !packed))
         return NYSTRA_ERR_NULL;
     const int eb = dtype_bytes(dtype), C = shape->channels;
     if (misaligned(X, eb) || misaligned(Wqkv, eb) || misaligned(Wproj, eb) || misaligned(Y, eb) ||
@@ -578,16 +574,28 @@ int nystra_block_forward(const void *X, const void *Wqkv, const void *bqkv, cons
         (bqkv && overlaps(workspace, wsb, bqkv, 3 * C * eb)) ||
         (bproj && overlaps(workspace, wsb, bproj, C * eb)))
         return NYSTRA_ERR_WORKSPACE;
+    if (use_packed) {   // read by the GEMMs only: no bytes shared with Y or the workspace
+        const int64_t pb = int64_t(bp.pk_qkv + bp.pk_proj);
+        if (misaligned(packed, 256))
+            return NYSTRA_ERR_ALIGN;
+        if (overlaps(packed, pb, Y, xb) || overlaps(packed, pb, workspace, wsb))
+            return NYSTRA_ERR_OVERLAP;
+    }
     char *ws = static_cast<char *>(workspace);
     void *q = ws, *k = ws + bp.qkvo_bytes, *v = ws + 2 * bp.qkvo_bytes,
          *o = ws + 3 * bp.qkvo_bytes;
-    char *pkq = bp.pk_qkv ? ws + 4 * bp.qkvo_bytes : nullptr;
-    char *pkp = bp.pk_qkv ? pkq + bp.pk_qkv : nullptr;
+    const char *pkq = nullptr, *pkp = nullptr;
+    if (bp.pk_qkv) {
+        pkq = use_packed ? static_cast<const char *>(packed) : ws + 4 * bp.qkvo_bytes;
+        pkp = pkq + bp.pk_qkv;
+    }
     char *attn_ws = ws + 4 * bp.qkvo_bytes + bp.pk_qkv + bp.pk_proj;
     hipStream_t st = static_cast<hipStream_t>(stream);
     clear_stale_error();
-    if (pkq) {
-        const hipError_t e = nystra::launch_block_wpack(Wqkv, Wproj, C, dtype, pkq, pkp, st);
+    if (pkq && !use_packed) {
+        const hipError_t e = nystra::launch_block_wpack(Wqkv, Wproj, C, dtype,
+                                                        const_cast<char *>(pkq),
+                                                        const_cast<char *>(pkp), st);
         if (e != hipSuccess)
             return finish_launch(e);
     }
@@ -634,6 +642,83 @@ int nystra_block_forward(const void *X, const void *Wqkv, const void *bqkv, cons
     g.out0 = Y;
     g.out1 = g.out2 = nullptr;
     return finish_launch(nystra::launch_block_gemm(g, st));
+}
+
+
+}  // namespace
+
+extern "C" {
+
+int nystra_block_workspace_size(const nystra_block_shape *shape, int m, int dtype,
+                                const nystra_opts *opts, int attention, size_t *bytes)
+{
+    if (!bytes)
+        return NYSTRA_ERR_NULL;
+    BlockPlan bp;
+    const int rc = plan_block(shape, m, dtype, opts, attention, &bp);
+    if (rc != NYSTRA_OK)
+        return rc;
+    *bytes = shape->batch == 0 ? 0 : bp.bytes;
+    return NYSTRA_OK;
+}
+
+int nystra_block_forward(const void *X, const void *Wqkv, const void *bqkv, const void *Wproj,
+                         const void *bproj, void *Y, const nystra_block_shape *shape, int m,
+                         int dtype, const nystra_opts *opts, int attention, void *workspace,
+                         size_t workspace_bytes, void *stream)
+{
+    return block_forward(X, Wqkv, bqkv, Wproj, bproj, false, nullptr, Y, shape, m, dtype,
+                         opts, attention, workspace, workspace_bytes, stream);
+}
+
+int nystra_block_packed_size(int channels, int dtype, size_t *bytes)
+{
+    if (!bytes)
+        return NYSTRA_ERR_NULL;
+    if (dtype != NYSTRA_F32 && dtype != NYSTRA_BF16)
+        return NYSTRA_ERR_DTYPE;
+    if (channels < 1 || channels > 4096)
+        return NYSTRA_ERR_SHAPE;
+    size_t q;
+    *bytes = packed_parts(channels, dtype, &q);
+    return NYSTRA_OK;
+}
+
+int nystra_block_pack_weights(const void *Wqkv, const void *Wproj, int channels, int dtype,
+                              void *packed, size_t packed_bytes, void *stream)
+{
+    size_t q = 0, need = 0;
+    const int rc = nystra_block_packed_size(channels, dtype, &need);
+    if (rc != NYSTRA_OK)
+        return rc;
+    if (need == 0)
+        return NYSTRA_OK;   // channels > 256: the block reads the weights as given
+    if (!Wqkv || !Wproj || !packed)
+        return NYSTRA_ERR_NULL;
+    const int eb = dtype_bytes(dtype);
+    if (misaligned(Wqkv, eb) || misaligned(Wproj, eb) || misaligned(packed, 256))
+        return NYSTRA_ERR_ALIGN;
+    if (packed_bytes < need)
+        return NYSTRA_ERR_WORKSPACE;
+    const int64_t C = channels;
+    if (overlaps(packed, int64_t(need), Wqkv, C * 3 * C * eb) ||
+        overlaps(packed, int64_t(need), Wproj, C * C * eb))
+        return NYSTRA_ERR_OVERLAP;
+    packed_parts(channels, dtype, &q);
+    char *pk = static_cast<char *>(packed);
+    clear_stale_error();
+    return finish_launch(nystra::launch_block_wpack(Wqkv, Wproj, channels, dtype, pk, pk + q,
+                                                    static_cast<hipStream_t>(stream)));
+}
+
+int nystra_block_forward_packed(const void *X, const void *Wqkv, const void *bqkv,
+                                const void *Wproj, const void *bproj, const void *packed,
+                                void *Y, const nystra_block_shape *shape, int m, int dtype,
+                                const nystra_opts *opts, int attention, void *workspace,
+                                size_t workspace_bytes, void *stream)
+{
+    return block_forward(X, Wqkv, bqkv, Wproj, bproj, true, packed, Y, shape, m, dtype, opts,
+                         attention, workspace, workspace_bytes, stream);
 }
 
 const char *nystra_status_str(int status)

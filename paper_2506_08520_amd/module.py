@@ -44,6 +44,7 @@ class NystraWindowAttention(nn.Module):
         self.w_proj = nn.Parameter(torch.empty(dim, dim, **kw), requires_grad=False)
         self.b_proj = nn.Parameter(torch.zeros(dim, **kw), requires_grad=False)
         self._ws = None
+        self._packed, self._packed_key = None, None
 
     @classmethod
     def from_linear(cls, qkv, proj, heads, window, shift=0, **kw):
@@ -69,6 +70,16 @@ class NystraWindowAttention(nn.Module):
             self._ws = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
         return self._ws, att
 
+    def _packed_weights(self):
+        """The GEMMs' packed image of w_qkv and w_proj, packed again only when
+        either weight changed (new storage, or an in-place update, which
+        advances the tensor's version counter)."""
+        key = tuple((t.data_ptr(), t._version, t.dtype) for t in (self.w_qkv, self.w_proj))
+        if key != self._packed_key:
+            self._packed = B.nystra_block_pack_weights(self.w_qkv, self.w_proj)
+            self._packed_key = key
+        return self._packed
+
     @torch.no_grad()
     def forward(self, x):
         if x.dim() != 4 or x.shape[-1] != self.dim:
@@ -77,7 +88,8 @@ class NystraWindowAttention(nn.Module):
         ws, att = self._workspace(x)
         return B.nystra_block_forward(x, self.w_qkv, self.b_qkv, self.w_proj, self.b_proj,
                                       self.heads, self.window, shift=self.shift, m=self.m,
-                                      opts=self.opts, attention=att, workspace=ws)
+                                      opts=self.opts, attention=att, workspace=ws,
+                                      packed=self._packed_weights())
 
 
 class SwinTransformerBlock(nn.Module):

@@ -323,3 +323,51 @@ def test_block_forward_validation(L):
     assert f(ws=ws + 64) == EWS
     assert f(ws=y) == EWS
     assert f(s=bshape(batch=0), x=None, y=None, ws=None) == OK
+
+
+def test_block_packed_size():
+    for C in (32, 96, 180, 256):
+        for bf16 in (False, True):
+            want = packed_weight_bytes(C, 3 * C, bf16) + packed_weight_bytes(C, C, bf16)
+            got = B.nystra_block_packed_size(C, B.BF16 if bf16 else B.F32)
+            assert got == want, (C, bf16)
+            # the block workspace reserves the same bytes for the per-call packing
+            heads = C // 16 if C % 16 == 0 else 6
+            plain = B.nystra_block_workspace_size(bshape(channels=C, heads=heads), 16,
+                                                  B.BF16 if bf16 else B.F32)
+            assert plain >= got
+    assert B.nystra_block_packed_size(288) == 0       # the block reads wider weights as given
+    n = ctypes.c_size_t(0)
+    assert B.lib().nystra_block_packed_size(96, 0, None) == ENULL
+    assert B.lib().nystra_block_packed_size(96, 7, ctypes.byref(n)) == EDTYPE
+    assert B.lib().nystra_block_packed_size(0, 0, ctypes.byref(n)) == ESHAPE
+    assert B.lib().nystra_block_packed_size(4097, 0, ctypes.byref(n)) == ESHAPE
+
+
+def test_block_pack_and_packed_forward_validation(L):
+    need = B.nystra_block_packed_size(96)
+    wq, wp, pk = P, P + (1 << 24), P + (2 << 24)
+    pack = L.nystra_block_pack_weights
+    assert pack(None, wp, 96, 0, pk, need, None) == ENULL
+    assert pack(wq, wp, 96, 0, None, need, None) == ENULL
+    assert pack(wq + 2, wp, 96, 0, pk, need, None) == EALIGN
+    assert pack(wq, wp, 96, 0, pk + 64, need, None) == EALIGN
+    assert pack(wq, wp, 96, 0, pk, need - 1, None) == EWS
+    assert pack(wq, wp, 96, 0, wp - 256, need, None) == EOVERLAP   # the image meets W_proj
+    assert pack(wq, wp, 96, 5, pk, need, None) == EDTYPE
+    assert pack(None, None, 288, 0, None, 0, None) == OK            # nothing to pack past 256
+
+    s = bshape()
+    nb = B.nystra_block_workspace_size(s, 16)
+    x, y, ws = P + (3 << 24), P + (4 << 24), P + (5 << 24)
+
+    def f(packed=pk, y=y, ws=ws, s=s):
+        return L.nystra_block_forward_packed(x, wq, None, wp, None, packed, y, ctypes.byref(s),
+                                             16, 0, None, 0, ws, nb, None)
+
+    assert f(packed=None) == ENULL
+    assert f(packed=pk + 64) == EALIGN
+    assert f(packed=y) == EOVERLAP
+    assert f(packed=ws) == EOVERLAP
+    assert f(ws=ws + 64) == EWS                  # the other checks are nystra_block_forward's
+    assert f(s=bshape(batch=0), packed=None) == OK

@@ -115,3 +115,48 @@ def test_block_weights_repacked_every_call(dtype):
                                dtype=dtype, round_output=False)
         check(y, ref, dtype, f"block with the weights of seed {seed}",
               beyond_bar=BLOCK_BEYOND_BF16)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("C,heads,w,s,m", [(96, 3, 8, 4, 16), (180, 6, 16, 8, 32)])
+def test_block_prepacked_weights(dtype, C, heads, w, s, m):
+    """nystra_block_forward_packed on an image packed once gives, bit for bit,
+    what nystra_block_forward gives with its per-call packing, on two inputs
+    in a row (one image, one workspace)."""
+    inp = W.block_inputs(1, 32, 32, C, seed=21, dtype=dtype)
+    other = W.block_inputs(1, 32, 32, C, seed=22, dtype=dtype)[0]
+    wq, bq, wp, bp = (to_dev(a, dtype) for a in inp[1:])
+    packed = B.nystra_block_pack_weights(wq, wp)
+    assert packed is not None and packed.numel() == B.nystra_block_packed_size(
+        C, B.F32 if dtype == "f32" else B.BF16)
+    for xh in (inp[0], other):
+        x = to_dev(xh, dtype)
+        y0 = B.nystra_block_forward(x, wq, bq, wp, bp, heads, w, shift=s, m=m)
+        y1 = B.nystra_block_forward(x, wq, bq, wp, bp, heads, w, shift=s, m=m, packed=packed)
+        torch.cuda.synchronize()
+        assert torch.equal(y0, y1)
+    ref = OB.block_forward(other, *inp[1:], heads=heads, window=w, shift=s, m=m, dtype=dtype,
+                           round_output=False)
+    check(to_host(y1), ref, dtype, "prepacked block", beyond_bar=BLOCK_BEYOND_BF16)
+
+
+def test_block_prepacked_not_needed_past_256_channels():
+    """Past 256 channels there is no image: packing is a no-op and the packed
+    forward takes a NULL image."""
+    C, heads = 288, 4
+    inp = W.block_inputs(1, 16, 16, C, seed=23, dtype="f32")
+    x, wq, bq, wp, bp = (to_dev(a, "f32") for a in inp)
+    assert B.nystra_block_packed_size(C) == 0
+    assert B.nystra_block_pack_weights(wq, wp) is None
+    y0 = B.nystra_block_forward(x, wq, bq, wp, bp, heads, 8, shift=4, m=16)
+    y1 = torch.empty_like(y0)
+    shape = B.BlockShape(1, 16, 16, C, heads, 8, 4)
+    need = B.nystra_block_workspace_size(shape, 16)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    rc = B.lib().nystra_block_forward_packed(
+        x.data_ptr(), wq.data_ptr(), bq.data_ptr(), wp.data_ptr(), bp.data_ptr(), None,
+        y1.data_ptr(), B.ctypes.byref(shape), 16, B.F32, None, B.BLOCK_NYSTROM, ws.data_ptr(),
+        need, None)
+    assert rc == 0
+    torch.cuda.synchronize()
+    assert torch.equal(y0, y1)

@@ -41,6 +41,28 @@ def test_window_attention_from_linear(attention):
     assert np.abs(y - ref).max() <= 1e-4
 
 
+def test_window_attention_repacks_after_weight_update():
+    """The module packs its projection weights once and reuses the image; an
+    in-place update of a weight (or new weights) is packed again."""
+    from paper_2506_08520_amd.module import NystraWindowAttention
+    C, heads, w, s = 96, 3, 8, 4
+    qkv, proj = linear_pair(C, 31)
+    mod = NystraWindowAttention.from_linear(qkv, proj, heads, w, s, m=16)
+    x = torch.randn(1, 16, 16, C, generator=torch.Generator().manual_seed(32)).cuda()
+    y0 = mod(x)
+    image = mod._packed
+    assert image is not None
+    assert torch.equal(mod(x), y0) and mod._packed is image    # reused, not repacked
+    qkv2, proj2 = linear_pair(C, 33)
+    with torch.no_grad():
+        mod.w_qkv.copy_(qkv2.weight.t())
+        mod.w_proj.copy_(proj2.weight.t())
+    y = to_host(mod(x))
+    ref = OB.block_forward(t2n(x), t2n(qkv2.weight).T, t2n(qkv.bias), t2n(proj2.weight).T,
+                           t2n(proj.bias), heads=heads, window=w, shift=s, m=16)
+    assert np.abs(y - ref).max() <= 1e-4
+
+
 def layer_norm(x, g, b, eps=1e-5):
     mu = x.mean(-1, keepdims=True)
     var = ((x - mu) ** 2).mean(-1, keepdims=True)
