@@ -248,7 +248,7 @@ struct RkLds {
     static constexpr int PF = 68;            // fp32 [k][c][t]: 64 floats + 4 per k
     static constexpr int PH = KP + 8;        // bf16 [n][k]: halves per column
     static constexpr int tile = BF ? 64 * PH / 2 : KP * PF;   // floats per buffer
-    static constexpr int astage = 16 * 8 * (KP / (BF ? 2 : 1) + 4);   // 128 rows, words
+    static constexpr int astage = 16 * 8 * (KP / (BF ? 2 : 1) + 8);   // 128 rows, words
     static constexpr int total = 2 * tile > astage ? 2 * tile : astage;
 };
 
@@ -343,7 +343,8 @@ __global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs 
     // k = g KQ + s -- into registers.  The stage shares LDS with the W tiles.
     constexpr int EPW = BF ? 2 : 1;              // elements per 4-byte word
     constexpr int AWL = KP / EPW;                // words per staged row
-    constexpr int AP = AWL + 4;                  // row pitch (words)
+    constexpr int AP = AWL + 8;                  // row pitch (words; + 8: fewer bank conflicts
+                                                 // than + 4 in the operand reads)
     __shared__ int rowbase[kRkRows];             // element offset of row r (-1: none)
     __shared__ int colofs[AWL];                  // element offset of word w in a row
     float *astage = lds_all;
