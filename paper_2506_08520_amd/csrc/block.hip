@@ -467,9 +467,7 @@ __global__ void __launch_bounds__(64 * kRkWaves) block_gemm_rk_kernel(BlockArgs 
 
     // Column part of the destination for the 64 columns of the current tile,
     // from out0: (QKV) output tensor `which` at which * ostride, head h,
-    // feature f -> h N d_h + f; (PROJ) the column.  The bias of every column
-    // is staged in LDS once: a global load in the epilogue would wait behind
-    // the next tile's W pieces in flight.
+    // feature f -> h N d_h + f; (PROJ) the column.
     __shared__ uint32_t coltab[2][64];
     auto cfill = [&](int ct, int buf) {
         if (tid < 64) {
