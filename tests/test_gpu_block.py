@@ -118,7 +118,8 @@ def test_block_weights_repacked_every_call(dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("C,heads,w,s,m", [(96, 3, 8, 4, 16), (180, 6, 16, 8, 32)])
+@pytest.mark.parametrize("C,heads,w,s,m", [(32, 1, 8, 4, 8), (96, 3, 8, 4, 16), (180, 6, 16, 8, 32),
+                                             (256, 8, 8, 4, 16)])
 def test_block_prepacked_weights(dtype, C, heads, w, s, m):
     """nystra_block_forward_packed on an image packed once gives, bit for bit,
     what nystra_block_forward gives with its per-call packing, on two inputs
