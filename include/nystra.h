@@ -241,9 +241,11 @@ int nystra_block_forward(const void *X, const void *Wqkv, const void *bqkv, cons
  * skipped: the GEMMs read `packed`, which must hold the image of the same
  * Wqkv and Wproj for these channels and dtype (its contents are not checked;
  * repack after changing the weights).  `packed` is required (NYSTRA_ERR_NULL)
- * for channels <= 256, ignored above; 256-byte aligned (NYSTRA_ERR_ALIGN) and
- * disjoint from Y and the workspace (NYSTRA_ERR_OVERLAP).  Every other
- * argument, the workspace size included, is as for nystra_block_forward.
+ * for channels <= 256, ignored above; `packed_bytes` at least
+ * nystra_block_packed_size (NYSTRA_ERR_WORKSPACE), 256-byte aligned
+ * (NYSTRA_ERR_ALIGN) and disjoint from Y and the workspace
+ * (NYSTRA_ERR_OVERLAP).  Every other argument, the workspace size included,
+ * is as for nystra_block_forward.
  * Results are identical to nystra_block_forward's. */
 int nystra_block_packed_size(int channels, int dtype, size_t *bytes);
 
@@ -252,9 +254,9 @@ int nystra_block_pack_weights(const void *Wqkv, const void *Wproj, int channels,
 
 int nystra_block_forward_packed(const void *X, const void *Wqkv, const void *bqkv,
                                 const void *Wproj, const void *bproj, const void *packed,
-                                void *Y, const nystra_block_shape *shape, int m, int dtype,
-                                const nystra_opts *opts, int attention, void *workspace,
-                                size_t workspace_bytes, void *stream);
+                                size_t packed_bytes, void *Y, const nystra_block_shape *shape,
+                                int m, int dtype, const nystra_opts *opts, int attention,
+                                void *workspace, size_t workspace_bytes, void *stream);
 
 /* Exact windowed softmax self-attention, Eq. (1), per unit:
  *   O = softmax(scale Q K^T) V, with the row maximum subtracted inside the

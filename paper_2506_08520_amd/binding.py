@@ -90,7 +90,8 @@ def lib():
                                               [ctypes.POINTER(Opts), _vp])
     L.nystra_block_packed_size.argtypes = [_i, _i, ctypes.POINTER(ctypes.c_size_t)]
     L.nystra_block_pack_weights.argtypes = [_vp, _vp, _i, _i, _vp, ctypes.c_size_t, _vp]
-    L.nystra_block_forward_packed.argtypes = ([_vp] * 7 + [ctypes.POINTER(BlockShape), _i, _i,
+    L.nystra_block_forward_packed.argtypes = ([_vp] * 6 + [ctypes.c_size_t, _vp,
+                                                           ctypes.POINTER(BlockShape), _i, _i,
                                                            ctypes.POINTER(Opts), _i, _vp,
                                                            ctypes.c_size_t, _vp])
     for name in EXPORTS:
@@ -245,7 +246,8 @@ def nystra_block_forward(x, w_qkv, b_qkv, w_proj, b_proj, heads, window, shift=0
         _check(rc, "nystra_block_forward")
     else:
         rc = lib().nystra_block_forward_packed(_ptr(x), _ptr(w_qkv), _ptr(b_qkv), _ptr(w_proj),
-                                               _ptr(b_proj), _ptr(packed), _ptr(y),
+                                               _ptr(b_proj), _ptr(packed),
+                                               packed.numel() * packed.element_size(), _ptr(y),
                                                ctypes.byref(shape), m, code, po, attention,
                                                _ptr(workspace), nbytes, _stream(stream))
         _check(rc, "nystra_block_forward_packed")

@@ -544,7 +544,8 @@ size_t packed_parts(int C, int dtype, size_t *qkv_part)
 // weight image at `packed` (required when channels <= 256, ignored above)
 // instead of packing W_qkv and W_proj into the workspace first.
 int block_forward(const void *X, const void *Wqkv, const void *bqkv, const void *Wproj,
-                  const void *bproj, bool with_packed, const void *packed, void *Y,
+                  const void *bproj, bool with_packed, const void *packed,
+                  size_t packed_bytes, void *Y,
                   const nystra_block_shape *shape, int m, int dtype, const nystra_opts *opts,
                   int attention, void *workspace, size_t workspace_bytes, void *stream)
 {
@@ -576,6 +577,8 @@ int block_forward(const void *X, const void *Wqkv, const void *bqkv, const void 
         return NYSTRA_ERR_WORKSPACE;
     if (use_packed) {   // read by the GEMMs only: no bytes shared with Y or the workspace
         const int64_t pb = int64_t(bp.pk_qkv + bp.pk_proj);
+        if (packed_bytes < size_t(pb))
+            return NYSTRA_ERR_WORKSPACE;
         if (misaligned(packed, 256))
             return NYSTRA_ERR_ALIGN;
         if (overlaps(packed, pb, Y, xb) || overlaps(packed, pb, workspace, wsb))
@@ -667,7 +670,7 @@ int nystra_block_forward(const void *X, const void *Wqkv, const void *bqkv, cons
                          int dtype, const nystra_opts *opts, int attention, void *workspace,
                          size_t workspace_bytes, void *stream)
 {
-    return block_forward(X, Wqkv, bqkv, Wproj, bproj, false, nullptr, Y, shape, m, dtype,
+    return block_forward(X, Wqkv, bqkv, Wproj, bproj, false, nullptr, 0, Y, shape, m, dtype,
                          opts, attention, workspace, workspace_bytes, stream);
 }
 
@@ -713,12 +716,12 @@ int nystra_block_pack_weights(const void *Wqkv, const void *Wproj, int channels,
 
 int nystra_block_forward_packed(const void *X, const void *Wqkv, const void *bqkv,
                                 const void *Wproj, const void *bproj, const void *packed,
-                                void *Y, const nystra_block_shape *shape, int m, int dtype,
-                                const nystra_opts *opts, int attention, void *workspace,
-                                size_t workspace_bytes, void *stream)
+                                size_t packed_bytes, void *Y, const nystra_block_shape *shape,
+                                int m, int dtype, const nystra_opts *opts, int attention,
+                                void *workspace, size_t workspace_bytes, void *stream)
 {
-    return block_forward(X, Wqkv, bqkv, Wproj, bproj, true, packed, Y, shape, m, dtype, opts,
-                         attention, workspace, workspace_bytes, stream);
+    return block_forward(X, Wqkv, bqkv, Wproj, bproj, true, packed, packed_bytes, Y, shape, m,
+                         dtype, opts, attention, workspace, workspace_bytes, stream);
 }
 
 const char *nystra_status_str(int status)

@@ -361,11 +361,12 @@ def test_block_pack_and_packed_forward_validation(L):
     nb = B.nystra_block_workspace_size(s, 16)
     x, y, ws = P + (3 << 24), P + (4 << 24), P + (5 << 24)
 
-    def f(packed=pk, y=y, ws=ws, s=s):
-        return L.nystra_block_forward_packed(x, wq, None, wp, None, packed, y, ctypes.byref(s),
-                                             16, 0, None, 0, ws, nb, None)
+    def f(packed=pk, pb=need, y=y, ws=ws, s=s):
+        return L.nystra_block_forward_packed(x, wq, None, wp, None, packed, pb, y,
+                                             ctypes.byref(s), 16, 0, None, 0, ws, nb, None)
 
     assert f(packed=None) == ENULL
+    assert f(pb=need - 1) == EWS
     assert f(packed=pk + 64) == EALIGN
     assert f(packed=y) == EOVERLAP
     assert f(packed=ws) == EOVERLAP

@@ -155,7 +155,7 @@ def test_block_prepacked_not_needed_past_256_channels():
     need = B.nystra_block_workspace_size(shape, 16)
     ws = torch.empty(need, dtype=torch.uint8, device="cuda")
     rc = B.lib().nystra_block_forward_packed(
-        x.data_ptr(), wq.data_ptr(), bq.data_ptr(), wp.data_ptr(), bp.data_ptr(), None,
+        x.data_ptr(), wq.data_ptr(), bq.data_ptr(), wp.data_ptr(), bp.data_ptr(), None, 0,
         y1.data_ptr(), B.ctypes.byref(shape), 16, B.F32, None, B.BLOCK_NYSTROM, ws.data_ptr(),
         need, None)
     assert rc == 0
