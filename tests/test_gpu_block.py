@@ -62,6 +62,9 @@ CASES = [
     (1, 64, 64, 64, 2, 64, 32, 16, "bf16", "nystrom"),
     (1, 16, 16, 256, 2, 8, 4, 16, "f32", "nystrom"),    # d_h = 128 (widest head)
     (1, 16, 24, 192, 2, 8, 0, 8, "bf16", "nystrom"),    # d_h = 96
+    # odd d_h (15) and 135 QKV columns: the GEMM epilogue stores single columns
+    (1, 16, 16, 45, 3, 8, 4, 16, "f32", "nystrom"),
+    (1, 16, 16, 45, 3, 8, 4, 16, "bf16", "nystrom"),
 ]
 
 
